@@ -1,0 +1,16 @@
+"""CPU oracle -- TEST INFRASTRUCTURE ONLY.
+
+Plain, slow, obviously correct reference implementations of what the HIP
+library computes, written from the paper (Libra, arXiv 2607.23250):
+
+* ``oracle.plan``      -- SH-Tiles (Eq. 5), tile cost (Eq. 6), KV groups
+  (Eq. 7), communication increment (Eq. 8) and the communication-aware
+  placement of Algorithm 2, in pure Python integers.
+* ``oracle.attention`` -- document-masked causal attention (Eq. 1 under the
+  block-diagonal causal mask of Sec. 2.3), forward and backward, in float64
+  NumPy, one sample and one head at a time.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  It shares no code with the HIP library
+and imports nothing from it; the product path never falls back to it.
+"""
