@@ -1,0 +1,273 @@
+#!/usr/bin/env python3
+"""Benchmark of the Libra hot path on one MI355X.
+
+One step = the whole path over one batch of synthetic input: plan the
+SH-Tiles (Eq. 6 costs + Algorithm 2, host C++), upload the tile list, run
+the packed causal attention forward and backward kernels for every tile set.
+The host plans step i+1 while the GPU runs step i, as the paper's
+asynchronous planner does.
+
+Default workload: one GPU's CP=16 head+tail share of a 1,048,576-token pack
+(Qwen3-30B-A3B attention: 32 query heads, 4 KV heads, head_dim 128; 65,536
+query rows against up to 1M causal keys, one ~900K-token sample), planned
+over 16 virtual workers.  ``--config k`` selects another of the five seeded
+workloads.  Inputs are seeded synthetic tensors resident in HBM before the
+timed region starts.
+
+Prints ONE JSON line: useful causal-masked attention TFLOP/s of fwd+bwd
+(4*d flops per causal same-sample (query, key) pair per query head forward,
+10*d backward), its fraction of the bf16 dense MFMA peak, the planner's
+max/mean worker load, the roofline entry of the dominant kernel (backward
+main kernel, timed with HIP events on its own stream) and the CPU oracle
+timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA: 4096 flop/clk/CU x 256 CU x 2.4 GHz
+METRIC = ("packed causal attention fwd+bwd useful TFLOP/s (and % bf16 MFMA peak); "
+          "max/mean tile load")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=5, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="time budget of the CPU oracle baseline (0 disables it)")
+    return ap.parse_args()
+
+
+def plan(pl, w, q_ranges=None):
+    return pl.libra_plan(w.lengths, w.pack_tokens, block_tokens=w.B, head_shards=w.H, cp=w.CP,
+                         num_q_heads=w.h_q, num_kv_heads=w.h_kv, head_dim=w.d, q_ranges=q_ranges)
+
+
+def launch_sets(w, full_tiles, share_tiles):
+    """Tile sets run as separate launches: one worker each for a pool (per-worker
+    execution), else the whole (share) tile list."""
+    if w.q_ranges is not None:
+        return [share_tiles]
+    if w.per_worker:
+        return [full_tiles[full_tiles["worker"] == r] for r in range(w.V)
+                if (full_tiles["worker"] == r).any()]
+    return [full_tiles]
+
+
+def traffic_entry(kernel: str, launches_per_step: int):
+    """HBM bytes per launch from committed rocprofv3 PMC summaries, or None when
+    missing or taken on a different kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    src = os.path.join(ROOT, "paper_2607_23250_amd", "csrc", rec.get("source", ""))
+    if not os.path.exists(src):
+        return None
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if sha != rec.get("source_sha256"):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(w, q, k, v, do, seconds):
+    """The oracle, as it stands, on a bounded random sample of query rows of the
+    same workload (all heads, forward + backward)."""
+    import torch
+    from oracle import attention as oa
+    pos = w.q_positions()
+    rng = np.random.default_rng(12345)
+    order = rng.permutation(len(pos))
+    done_rows = []
+    t0 = time.perf_counter()
+    i = 0
+    while time.perf_counter() - t0 < seconds and i < len(order):
+        rows = np.sort(order[i:i + 2])
+        i += 2
+        oa.attention_fwd(q, k, v, w.lengths, pos, rows=rows)
+        oa.attention_bwd(q, k, v, do, w.lengths, pos, rows=rows)
+        done_rows.extend(rows.tolist())
+    dt = time.perf_counter() - t0
+    pairs = oa.useful_pairs(w.lengths, pos[np.asarray(done_rows, dtype=np.int64)])
+    flops = 14.0 * w.d * w.h_q * pairs
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": torch.get_num_threads(),
+            "kind": "oracle",
+            "sample": (f"{len(done_rows)} random query rows of {len(pos)} x {w.h_q} heads, "
+                       f"fwd+bwd in float64 ({pairs} causal pairs per head, {dt:.1f} s)")}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the multi-GPU exchange of the paper is out of scope here)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2607_23250_amd as pl
+    import workloads as wl
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    w = wl.config(args.config)
+    full_tiles, loads = plan(pl, w)
+    share_tiles = plan(pl, w, w.q_ranges)[0] if w.q_ranges is not None else None
+    sets = launch_sets(w, full_tiles, share_tiles)
+    cost = sum(int(s["cost"].sum()) for s in sets)            # = h_q * causal pairs
+    fwd_flops = 4.0 * w.d * cost
+    bwd_flops = 10.0 * w.d * cost
+    max_over_mean = float(w.V * loads.max() / loads.sum())
+
+    # inputs resident in HBM
+    q, k, v, do = wl.tensors(w.seed, w.n_q_rows, w.n_kv_rows, w.h_q, w.h_kv, w.d)
+    qd, kd, vd, dod = (t.to(dev) for t in (q, k, v, do))
+    cu = np.zeros(len(w.lengths) + 1, dtype=np.int64)
+    cu[1:] = np.cumsum(w.lengths)
+    cud = torch.from_numpy(cu).to(dev)
+    o = torch.empty_like(qd)
+    lse = torch.empty((w.h_q, w.n_q_rows), dtype=torch.float32, device=dev)
+    dq = torch.empty_like(qd)
+    acc = len(sets) > 1
+    kv_dtype = torch.float32 if acc else torch.bfloat16
+    dk = torch.zeros(kd.shape, dtype=kv_dtype, device=dev)
+    dv = torch.zeros(kd.shape, dtype=kv_dtype, device=dev)
+    n = len(w.lengths)
+    ws_bytes = max(max(pl.libra_attn_workspace_size(len(s), n, w.n_q_rows, w.n_kv_rows, w.h_q,
+                                                    w.h_kv, w.d, b) for b in (False, True))
+                   for s in sets)
+    ws = pl.alloc_workspace(ws_bytes, dev)
+    tile_bytes = [len(s) * pl.TILE_DTYPE.itemsize for s in sets]
+    dev_tiles = [torch.empty(b, dtype=torch.uint8, device=dev) for b in tile_bytes]
+    host_tiles = [[torch.empty(b, dtype=torch.uint8, pin_memory=True) for b in tile_bytes]
+                  for _ in range(2)]
+    copied = [None, None]
+    stream = torch.cuda.current_stream(dev)
+    plan_ms = []
+
+    def make_plan(buf):
+        """Plan on the host into pinned buffer `buf` (the tile sets of the step)."""
+        if copied[buf] is not None:
+            copied[buf].synchronize()
+        t0 = time.perf_counter()
+        ft, _ = plan(pl, w)
+        st = plan(pl, w, w.q_ranges)[0] if w.q_ranges is not None else None
+        plan_ms.append((time.perf_counter() - t0) * 1e3)
+        for h, s in zip(host_tiles[buf], launch_sets(w, ft, st)):
+            h.numpy()[:] = np.ascontiguousarray(s).view(np.uint8)
+
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    split_ms = []
+
+    def step(i, record):
+        buf = i % 2
+        for d_t, h_t in zip(dev_tiles, host_tiles[buf]):
+            d_t.copy_(h_t, non_blocking=True)
+        copied[buf] = torch.cuda.Event()
+        copied[buf].record(stream)
+        if acc:
+            dk.zero_()
+            dv.zero_()
+        if record:
+            ev[0].record(stream)
+        for td in dev_tiles:
+            pl.libra_attn_fwd(qd, kd, vd, cud, td, o=o, lse=lse, workspace=ws)
+        if record:
+            ev[1].record(stream)
+        for td in dev_tiles:
+            pl.libra_attn_bwd(qd, kd, vd, o, lse, dod, cud, td, dq=dq, dk=dk, dv=dv,
+                              accumulate=acc, workspace=ws)
+        if record:
+            ev[2].record(stream)
+        make_plan((i + 1) % 2)          # host plans the next step while the GPU runs
+
+    make_plan(0)
+    for i in range(args.warmup):
+        step(i, False)
+    torch.cuda.synchronize()
+    # one step with fwd / bwd split events (not part of the timed region)
+    step(args.warmup, True)
+    torch.cuda.synchronize()
+    split_ms = (ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]))
+
+    pl.libra_timing_enable(True)
+    plan_ms.clear()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + 1 + i, False)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    fwd_main_ms, n_fwd = pl.libra_timing_read(0)
+    bwd_main_ms, n_bwd = pl.libra_timing_read(1)
+    pl.libra_timing_enable(False)
+
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    value = (fwd_flops + bwd_flops) / (ms_per_step * 1e-3) / 1e12
+    bwd_launch_ms = bwd_main_ms / max(n_bwd, 1)
+    bwd_launch_flops = bwd_flops / len(sets)
+    achieved = bwd_launch_flops / (bwd_launch_ms * 1e-3) / 1e12
+    fwd_achieved = (fwd_flops / len(sets)) / (fwd_main_ms / max(n_fwd, 1) * 1e-3) / 1e12
+    traffic = traffic_entry("attn_bwd_kernel", len(sets))
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "pack_tokens": w.pack_tokens if w.P <= 2 else [w.pack_tokens[0]] * w.P,
+            "query_rows": w.n_q_rows, "kv_rows": w.n_kv_rows, "samples": len(w.lengths),
+            "max_sample": max(w.lengths), "h_q": w.h_q, "h_kv": w.h_kv, "head_dim": w.d,
+            "block_tokens": w.B, "head_shards": w.H, "cp": w.CP, "virtual_workers": w.V,
+            "launches_per_step": len(sets), "tiles_executed": int(sum(len(s) for s in sets)),
+            "assumptions": w.notes,
+        },
+        "pct_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "max_over_mean_load": round(max_over_mean, 4),
+        "useful_tflop_per_step": round((fwd_flops + bwd_flops) / 1e12, 3),
+        "fwd_ms": round(split_ms[0], 3),
+        "bwd_ms": round(split_ms[1], 3),
+        "fwd_tflops": round(fwd_flops / (split_ms[0] * 1e-3) / 1e12, 1),
+        "bwd_tflops": round(bwd_flops / (split_ms[1] * 1e-3) / 1e12, 1),
+        "fwd_main_kernel_tflops": round(fwd_achieved, 1),
+        "plan_ms": round(float(np.mean(plan_ms)), 3) if plan_ms else None,
+        "roofline": {
+            "kernel": "attn_bwd_kernel<128>",
+            "bound": "mfma",
+            "achieved": round(achieved, 1),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic,
+            "launch_ms": round(bwd_launch_ms, 3),
+            "flops_per_launch": bwd_launch_flops,
+        },
+    }
+    if args.cpu_seconds > 0:
+        out["cpu_baseline"] = cpu_baseline(w, q, k, v, do, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,122 @@
+"""libra_plan (C++) against the plan oracle: bit-exact tiles, costs,
+placement and loads on the five workloads and on random small inputs; error
+paths forced from the host."""
+import numpy as np
+import pytest
+
+import paper_2607_23250_amd as pl
+from oracle import plan as op
+import workloads as wl
+
+
+def _native(w, q_ranges=None, **over):
+    kw = dict(block_tokens=w.B, head_shards=w.H, cp=w.CP, num_q_heads=w.h_q,
+              num_kv_heads=w.h_kv, head_dim=w.d)
+    kw.update(over)
+    return pl.libra_plan(w.lengths, w.pack_tokens, q_ranges=q_ranges, **kw)
+
+
+def _oracle(w, q_ranges=None, elem_bytes=2, tau=(3, 100)):
+    cfg = op.PlanCfg(B=w.B, H=w.H, P=w.P, CP=w.CP, h_q=w.h_q, h_kv=w.h_kv, d=w.d,
+                     elem_bytes=elem_bytes, tau_num=tau[0], tau_den=tau[1])
+    return op.plan(cfg, w.lengths, w.pack_tokens, q_ranges)
+
+
+def _same(native, oracle):
+    tiles, loads = native
+    otiles, oloads = oracle
+    assert len(tiles) == len(otiles)
+    for a, b in zip(tiles, otiles):
+        got = (int(a["id"]), int(a["pack"]), int(a["q_begin"]), int(a["q_end"]), int(a["q_row"]),
+               int(a["cost"]), int(a["head_begin"]), int(a["head_end"]), int(a["home"]),
+               int(a["worker"]))
+        want = (b.id, b.pack, b.q_begin, b.q_end, b.q_row, b.cost, b.head_begin, b.head_end,
+                b.home, b.worker)
+        assert got == want
+    assert [int(x) for x in loads] == list(oloads)
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_configs_bit_exact(k):
+    w = wl.config(k)
+    _same(_native(w), _oracle(w))
+    if w.q_ranges is not None:
+        _same(_native(w, w.q_ranges), _oracle(w, w.q_ranges))
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_configs_meet_load_target(k):
+    w = wl.config(k)
+    tiles, loads = _native(w)
+    assert w.V * loads.max() / loads.sum() <= 1.05
+
+
+@pytest.mark.parametrize("seed", range(300))
+def test_random_small_bit_exact(seed):
+    w = wl.tiny_random(seed, max_packs=4, max_len=96)
+    rng = np.random.default_rng(seed)
+    tau = (int(rng.integers(0, 20)), int(rng.integers(1, 200)))
+    eb = int(rng.choice([1, 2, 4]))
+    _same(_native(w, elem_bytes=eb, tau=tau), _oracle(w, elem_bytes=eb, tau=tau))
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_q_ranges_bit_exact(seed):
+    w = wl.tiny_random(seed + 1000, max_packs=3, max_len=96)
+    rng = np.random.default_rng(seed)
+    # whole blocks of each pack, chosen at random, merged into sorted ranges
+    blocks = []
+    off = 0
+    for L in w.pack_tokens:
+        for lo in range(off, off + L, w.B):
+            blocks.append((lo, min(off + L, lo + w.B)))
+        off += L
+    keep = [b for b in blocks if rng.random() < 0.5] or blocks[:1]
+    ranges = []
+    for b, e in keep:
+        if ranges and ranges[-1][1] == b:
+            ranges[-1] = (ranges[-1][0], e)
+        else:
+            ranges.append((b, e))
+    _same(_native(w, ranges), _oracle(w, ranges))
+
+
+def test_size_query_and_enospc():
+    w = wl.config(2)
+    tiles, _ = _native(w)
+    import ctypes
+    L = pl.lib()
+    lengths = np.asarray(w.lengths, dtype=np.int64)
+    cu = pl._offsets(lengths)
+    pcu = pl._offsets(w.pack_tokens)
+    cfg = pl._PlanCfg(w.B, w.H, w.P, w.CP, w.h_q, w.h_kv, w.d, 2, 3, 100)
+    n = ctypes.c_int64(-1)
+    out = np.zeros(3, dtype=pl.TILE_DTYPE)
+    rc = L.libra_plan(ctypes.byref(cfg), pl._ptr(lengths), len(lengths), pl._ptr(cu), pl._ptr(pcu),
+                      None, 0, pl._ptr(out), 3, ctypes.byref(n), None)
+    assert rc == pl.LIBRA_ENOSPC and n.value == len(tiles)
+
+
+def _expect(code, **kw):
+    with pytest.raises(pl.LibraError) as e:
+        pl.libra_plan(**kw)
+    assert e.value.code == code
+
+
+def test_error_paths():
+    base = dict(lengths=[3, 5], pack_tokens=[8], block_tokens=4, head_shards=2, cp=1,
+                num_q_heads=4, num_kv_heads=2, head_dim=64)
+    pl.libra_plan(**base)
+    _expect(pl.LIBRA_EINVAL, **{**base, "head_shards": 3})              # H does not divide h_q
+    _expect(pl.LIBRA_EINVAL, **{**base, "num_kv_heads": 3})             # h_kv does not divide h_q
+    _expect(pl.LIBRA_EINVAL, **{**base, "lengths": [3, 0, 5]})          # empty sample
+    _expect(pl.LIBRA_EINVAL, **{**base, "pack_tokens": [4, 4]})         # pack cuts a sample
+    _expect(pl.LIBRA_EINVAL, **{**base, "cp": 3})                       # 8 % 6 != 0
+    _expect(pl.LIBRA_EINVAL, **{**base, "q_ranges": [(1, 4)]})          # not whole blocks
+    _expect(pl.LIBRA_EINVAL, **{**base, "q_ranges": [(4, 8), (0, 4)]})  # unsorted
+    _expect(pl.LIBRA_EINVAL, **{**base, "block_tokens": 0})
+    _expect(pl.LIBRA_EINVAL, **{**base, "tau": (3, 0)})
+    _expect(pl.LIBRA_EINVAL, **{**base, "head_shards": 4, "num_kv_heads": 3, "num_q_heads": 12})
+    # costs beyond int64: one sample of 2^32 tokens with 2^31 heads per shard
+    _expect(pl.LIBRA_EOVERFLOW, lengths=[1 << 32], pack_tokens=[1 << 32], block_tokens=1 << 30,
+            head_shards=1, cp=1, num_q_heads=1 << 30, num_kv_heads=1, head_dim=64)

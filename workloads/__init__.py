@@ -245,3 +245,31 @@ def tiny_random(seed: int, max_packs: int = 3, max_len: int = 40,
         packs.append(lens)
     B = int(rng.integers(1, max(2, max(sum(p) for p in packs)) + 1))
     return Workload(f"tiny{seed}", seed, packs, h_q, h_kv, d, B=B, H=H, CP=CP)
+
+
+def small_random(seed: int) -> Workload:
+    """A few-hundred-token random pool that spans several kernel tiles.
+
+    Ragged sample and pack sizes, block sizes that are not multiples of the
+    kernel's row or key blocks, and head layouts from MHA to 16-way GQA.
+    """
+    rng = np.random.default_rng(20_000 + seed)
+    layouts = [(2, 1, 2), (4, 1, 2), (8, 2, 2), (8, 2, 4), (16, 2, 2), (32, 4, 2), (12, 4, 4),
+               (4, 4, 1), (32, 2, 8), (6, 3, 3)]
+    h_q, h_kv, H = layouts[int(rng.integers(0, len(layouts)))]
+    d = int(rng.choice([64, 128]))
+    CP = int(rng.choice([1, 2]))
+    P = int(rng.integers(1, 4))
+    packs = []
+    for _ in range(P):
+        L = 2 * CP * int(rng.integers(8, 160))
+        lens: List[int] = []
+        room = L
+        while room > 0:
+            n = min(int(rng.integers(1, 400)) if rng.random() < 0.8 else int(rng.integers(1, 8)),
+                    room)
+            lens.append(n)
+            room -= n
+        packs.append(lens)
+    B = int(rng.integers(1, 300))
+    return Workload(f"small{seed}", seed, packs, h_q, h_kv, d, B=B, H=H, CP=CP)
