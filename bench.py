@@ -210,16 +210,20 @@ def main():
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     fwd_main_ms, n_fwd = pl.libra_timing_read(0)
-    bwd_main_ms, n_bwd = pl.libra_timing_read(1)
+    kv_ms, n_kv = pl.libra_timing_read(1)
+    dq_ms, n_dq = pl.libra_timing_read(2)
     pl.libra_timing_enable(False)
 
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     value = (fwd_flops + bwd_flops) / (ms_per_step * 1e-3) / 1e12
-    bwd_launch_ms = bwd_main_ms / max(n_bwd, 1)
-    bwd_launch_flops = bwd_flops / len(sets)
-    achieved = bwd_launch_flops / (bwd_launch_ms * 1e-3) / 1e12
+    # dominant kernel: the backward dK/dV kernel; its algorithmic work is the
+    # S, dP, dV and dK contractions, 8*d flops per causal pair per query head
+    kv_launch_ms = kv_ms / max(n_kv, 1)
+    kv_launch_flops = 8.0 * w.d * cost / len(sets)
+    achieved = kv_launch_flops / (kv_launch_ms * 1e-3) / 1e12
+    dq_launch_ms = dq_ms / max(n_dq, 1)
     fwd_achieved = (fwd_flops / len(sets)) / (fwd_main_ms / max(n_fwd, 1) * 1e-3) / 1e12
-    traffic = traffic_entry("attn_bwd_kernel", len(sets))
+    traffic = traffic_entry("attn_bwd_dkdv_kernel", len(sets))
 
     out = {
         "metric": METRIC,
@@ -251,17 +255,21 @@ def main():
         "fwd_tflops": round(fwd_flops / (split_ms[0] * 1e-3) / 1e12, 1),
         "bwd_tflops": round(bwd_flops / (split_ms[1] * 1e-3) / 1e12, 1),
         "fwd_main_kernel_tflops": round(fwd_achieved, 1),
+        "bwd_dkdv_kernel_ms": round(kv_launch_ms, 3),
+        "bwd_dq_kernel_ms": round(dq_launch_ms, 3),
+        "bwd_dq_kernel_useful_tflops": round(2.0 * w.d * cost / len(sets) / (dq_launch_ms * 1e-3)
+                                             / 1e12, 1),
         "plan_ms": round(float(np.mean(plan_ms)), 3) if plan_ms else None,
         "roofline": {
-            "kernel": "attn_bwd_kernel<128>",
+            "kernel": f"attn_bwd_dkdv_kernel<{w.d}>",
             "bound": "mfma",
             "achieved": round(achieved, 1),
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic,
-            "launch_ms": round(bwd_launch_ms, 3),
-            "flops_per_launch": bwd_launch_flops,
+            "launch_ms": round(kv_launch_ms, 3),
+            "flops_per_launch": kv_launch_flops,
         },
     }
     if args.cpu_seconds > 0:

@@ -177,11 +177,12 @@ int libra_attn_bwd(const void *q, const void *k, const void *v, const void *o, c
  * Kernel timing (tracing aid).  libra_timing_enable(1) clears the records of
  * the calling thread and makes every later libra_attn_fwd / libra_attn_bwd
  * call on that thread record HIP events on its stream around its main
- * persistent kernel (the work-item kernels, not the small preparation
+ * persistent kernels (the work-item kernels, not the small preparation
  * passes); libra_timing_enable(0) stops recording.  libra_timing_read waits
  * for the recorded events and returns the summed milliseconds and the number
- * of launches of the forward (which = 0) or backward (which = 1) main kernel
- * since the last enable.  Errors: EINVAL (bad `which`, NULL outputs), EHIP.
+ * of launches since the last enable of: which = 0, the forward kernel;
+ * 1, the backward dK/dV kernel; 2, the backward dQ kernel.
+ * Errors: EINVAL (bad `which`, NULL outputs), EHIP.
  */
 int libra_timing_enable(int enable);
 int libra_timing_read(int which, double *total_ms, int64_t *launches);

@@ -142,7 +142,8 @@ def libra_timing_enable(enable: bool = True) -> None:
 
 
 def libra_timing_read(which: int) -> Tuple[float, int]:
-    """(summed milliseconds, launches) of the forward (0) / backward (1) main kernel."""
+    """(summed milliseconds, launches) of the forward kernel (0), the backward
+    dK/dV kernel (1) or the backward dQ kernel (2)."""
     ms = ctypes.c_double(0.0)
     n = ctypes.c_int64(0)
     _check(lib().libra_timing_read(which, ctypes.byref(ms), ctypes.byref(n)), "libra_timing_read")

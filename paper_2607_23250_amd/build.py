@@ -34,6 +34,9 @@ def hip_flags():
     return [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-munsafe-fp-atomics",
             # no packed-fp32 instructions anywhere in the device code
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+            # MFMA accumulators in VGPRs: the default heuristic shuffles them
+            # through AGPRs inside the hot loops of the occupancy-1 kernels
+            "-mllvm", "--amdgpu-mfma-vgpr-form=1",
             f"-I{INCLUDE}", f"-I{CSRC}"]
 
 

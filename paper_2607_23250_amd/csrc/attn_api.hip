@@ -41,8 +41,8 @@ int check_ws(const void *ws, size_t bytes, size_t need) {
 // from a thread-exit destructor could run after the HIP runtime is gone).
 struct Timing {
   bool on = false;
-  std::vector<KernelTimer> ev[2];
-  size_t used[2] = {0, 0};
+  std::vector<KernelTimer> ev[3];
+  size_t used[3] = {0, 0, 0};
 };
 Timing &timing() {
   static thread_local Timing t;
@@ -71,13 +71,13 @@ const KernelTimer *next_timer(int which, int *rc) {
 extern "C" int libra_timing_enable(int enable) {
   Timing &t = timing();
   t.on = enable != 0;
-  t.used[0] = t.used[1] = 0;
+  t.used[0] = t.used[1] = t.used[2] = 0;
   return LIBRA_OK;
 }
 
 extern "C" int libra_timing_read(int which, double *total_ms, int64_t *launches) {
-  if ((which != 0 && which != 1) || !total_ms || !launches)
-    return fail(LIBRA_EINVAL, "libra_timing_read: which must be 0 or 1, outputs non-NULL");
+  if (which < 0 || which > 2 || !total_ms || !launches)
+    return fail(LIBRA_EINVAL, "libra_timing_read: which must be 0, 1 or 2, outputs non-NULL");
   Timing &t = timing();
   double sum = 0.0;
   for (size_t i = 0; i < t.used[which]; ++i) {
@@ -147,10 +147,12 @@ extern "C" int libra_attn_bwd(const void *q, const void *k, const void *v, const
     if (int rc = check_ws(workspace, workspace_bytes, L.total)) return rc;
   const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt((float)head_dim);
   int rc = LIBRA_OK;
-  const KernelTimer *tm = num_tiles > 0 ? next_timer(1, &rc) : nullptr;
+  const KernelTimer *tm_kv = num_tiles > 0 ? next_timer(1, &rc) : nullptr;
+  if (rc) return rc;
+  const KernelTimer *tm_q = num_tiles > 0 ? next_timer(2, &rc) : nullptr;
   if (rc) return rc;
   return launch_bwd(q, k, v, o, lse, dout, cu_seqlens, num_samples, tiles, num_tiles, n_q_rows,
                     n_kv_rows, h_q, h_kv, head_dim, scale, dq, dk, dv,
                     (flags & LIBRA_BWD_ACCUMULATE_DKV) != 0, workspace, L,
-                    static_cast<hipStream_t>(stream), tm);
+                    static_cast<hipStream_t>(stream), tm_kv, tm_q);
 }

@@ -5,21 +5,24 @@
 // these): P = exp(S - LSE), D = rowsum(dO * O), dV = P^T dO,
 // dS = P * (dO V^T - D), dQ = scale dS K, dK = scale dS^T Q.
 //
-// Structure:
-//   * a pre-pass writes D, transposed copies Q^T / dO^T of the covered rows
-//     (so every MFMA operand is read from LDS as 16 contiguous bytes) and
-//     clears the fp32 dQ accumulator;
-//   * one workgroup prepares KV-block work items, longest-first;
-//   * a persistent KV-stationary kernel: a work item is 128 keys of one KV
-//     head of one sample (anchored at the sample start); each of the 4 waves
-//     keeps 32 keys of K and V in registers plus fp32 dK^T / dV^T
-//     accumulators, and loops over the 32-row query blocks of the tiles that
-//     attend them and over the query heads of the KV group.  S and dP are
-//     computed with queries on M (lane = key), which is exactly the operand
-//     layout dV^T = dO^T P and dK^T = Q^T dS need; dS goes through LDS once
-//     so that dQ = dS K over all 128 keys is one contraction per wave,
-//     accumulated into fp32 with hardware float atomics;
-//   * a finalize pass converts dQ to bf16 for the covered rows and heads.
+// Two persistent kernels, no atomics (every output element has one writer):
+//   * dK / dV, KV-stationary: a work item is 128 keys of one KV head of one
+//     sample (anchored at the sample start); each of the 4 waves keeps 32 keys
+//     of K and V in registers plus fp32 dK^T / dV^T accumulators and loops
+//     over the 32-row query blocks of the tiles that attend them and over the
+//     query heads of the KV group.  S and dP are computed with queries on M
+//     (lane = key), exactly the operand layout that dV^T = dO^T P and
+//     dK^T = Q^T dS need.  Query blocks are staged in LDS double-buffered,
+//     the next one loaded while the current one is computed.
+//   * dQ, query-stationary, shaped like the forward: S^T = K Q^T and
+//     dP^T = V dO^T (lane = query), dS^T = P^T * (dP^T - D), then
+//     dQ^T += K^T dS^T.  It recomputes S and dP instead of accumulating dQ
+//     across key blocks with atomics: on long samples that accumulation is
+//     read-modify-write traffic of 4 bytes x d per (32 queries x 128 keys)
+//     per head, which would bound the whole backward by HBM.
+// Preparation: D = rowsum(dO * O), transposed Q^T / dO^T of the covered rows
+// and a padded transposed K^T (every MFMA operand is read from LDS as 16
+// contiguous bytes), plus the two work-item lists, longest first.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -47,28 +50,27 @@ __device__ __forceinline__ unsigned long long group_bits(int hb, int he, int G) 
 // ---------------------------------------------------------------------------
 // One workgroup: per sample, the key extent attended by covered rows and the
 // KV heads involved; then items (sample, 128-key block, KV head) ordered by
-// the number of attending rows, longest first.
+// the number of attending rows, longest first, one queue per XCD keyed by
+// (KV head, key block) so that an XCD streams the query blocks of few heads.
 __global__ __launch_bounds__(kPrepThreads) void prep_bwd_kernel(
     const int64_t *__restrict__ cu, int64_t n, const libra_tile_t *__restrict__ tiles, int64_t T,
     int h_q, int h_kv, int64_t n_q, int64_t n_kv, int32_t *__restrict__ hdr,
     int32_t *__restrict__ ext, unsigned long long *__restrict__ gmask,
     BwdItem *__restrict__ items, int64_t max_items) {
-  __shared__ int32_t hist[kBuckets];
+  __shared__ int32_t hist[kXcds * kQBuckets];
   __shared__ int32_t part[kPrepThreads];
-  __shared__ int32_t bad;
   const int tid = threadIdx.x;
   const int G = h_q / h_kv;
+  const int R = h_kv >= kXcds ? 1 : kXcds / h_kv;
   for (int64_t j = tid; j < n; j += kPrepThreads) {
     __hip_atomic_store(&ext[j], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&gmask[j], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  for (int i = tid; i < kBuckets; i += kPrepThreads) hist[i] = 0;
-  if (tid == 0) bad = 0;
   __threadfence();
   __syncthreads();
   for (int64_t t = tid; t < T; t += kPrepThreads) {
     const libra_tile_t tl = tiles[t];
-    if (!tile_ok(tl, n_q, n_kv, h_q)) { atomicAdd(&bad, 1); continue; }
+    if (!tile_ok(tl, n_q, n_kv, h_q)) continue;
     const unsigned long long bits = group_bits(tl.head_begin, tl.head_end, G);
     for (int64_t j = upper_bound64(cu, n, tl.q_begin) - 1; j < n && cu[j] < tl.q_end; ++j) {
       const int64_t pe = tl.q_end < cu[j + 1] ? tl.q_end : cu[j + 1];
@@ -78,70 +80,32 @@ __global__ __launch_bounds__(kPrepThreads) void prep_bwd_kernel(
   }
   __threadfence();
   __syncthreads();
-  auto bucket = [](int32_t e, int kb) {
-    const int32_t c = (e - kb * kBwdBK + kRows - 1) / kRows;   // attending row blocks
-    return kBuckets - (c < kBuckets ? c : kBuckets);
+  auto each = [&](auto &&f) {
+    for (int64_t j = tid; j < n; j += kPrepThreads) {
+      const int32_t e = ld_agent(&ext[j]);
+      if (e == 0) continue;
+      const unsigned long long mk = ld_agent(&gmask[j]);
+      const int nkb = (e + kBwdBK - 1) / kBwdBK;
+      for (int g = 0; g < h_kv; ++g)
+        if (mk >> g & 1ull)
+          for (int kb = 0; kb < nkb; ++kb)
+            f(BwdItem{(int32_t)j, kb, g, 0}, (int64_t)(e - kb * kBwdBK + kRows - 1) / kRows,
+              (g * R + kb % R) % kXcds);
+    }
   };
-  for (int64_t j = tid; j < n; j += kPrepThreads) {
-    const int32_t e = ld_agent(&ext[j]);
-    if (e == 0) continue;
-    const unsigned long long mk = ld_agent(&gmask[j]);
-    const int nkb = (e + kBwdBK - 1) / kBwdBK;
-    for (int g = 0; g < h_kv; ++g)
-      if (mk >> g & 1ull)
-        for (int kb = 0; kb < nkb; ++kb) atomicAdd(&hist[bucket(e, kb)], 1);
-  }
-  __syncthreads();
-  constexpr int per = kBuckets / kPrepThreads;
-  int32_t s = 0;
-  for (int i = 0; i < per; ++i) s += hist[tid * per + i];
-  part[tid] = s;
-  __syncthreads();
-  for (int o = 1; o < kPrepThreads; o <<= 1) {
-    const int32_t v = tid >= o ? part[tid - o] : 0;
-    __syncthreads();
-    part[tid] += v;
-    __syncthreads();
-  }
-  int32_t base = part[tid] - s;
-  const int32_t total = part[kPrepThreads - 1];
-  __syncthreads();
-  for (int i = 0; i < per; ++i) {
-    const int32_t c = hist[tid * per + i];
-    hist[tid * per + i] = base;
-    base += c;
-  }
-  __syncthreads();
-  for (int64_t j = tid; j < n; j += kPrepThreads) {
-    const int32_t e = ld_agent(&ext[j]);
-    if (e == 0) continue;
-    const unsigned long long mk = ld_agent(&gmask[j]);
-    const int nkb = (e + kBwdBK - 1) / kBwdBK;
-    for (int g = 0; g < h_kv; ++g)
-      if (mk >> g & 1ull)
-        for (int kb = 0; kb < nkb; ++kb) {
-          const int32_t pos = atomicAdd(&hist[bucket(e, kb)], 1);
-          if (pos < max_items) items[pos] = BwdItem{(int32_t)j, kb, g, 0};
-        }
-  }
-  if (tid == 0) {
-    hdr[kBwdQueue] = 0;
-    hdr[kBwdItems] = total < max_items ? total : (int32_t)max_items;
-    hdr[kBadTiles] = bad + (total > max_items ? 1 : 0);
-  }
+  build_queues<BwdItem>(each, hist, part, hdr, kBwdQ, items, max_items);
 }
 
 // ---------------------------------------------------------------------------
 // Pre-pass over the covered (row, head) pairs, 32 rows at a time:
-// D = rowsum(dO * O), Q^T and dO^T as [h_q][D][nq_pad], dQ accumulator = 0.
+// D = rowsum(dO * O) and Q^T, dO^T as [h_q][D][nq_pad].
 constexpr int kTileSplit = 64;
 
 template <int D>
 __global__ __launch_bounds__(256) void bwd_pre_kernel(
     const bf16 *__restrict__ q, const bf16 *__restrict__ o, const bf16 *__restrict__ dout,
     const libra_tile_t *__restrict__ tiles, int h_q, int64_t n_q, int64_t n_kv, int64_t nq_pad,
-    float *__restrict__ dvec, bf16 *__restrict__ qt, bf16 *__restrict__ dot,
-    float *__restrict__ dqacc) {
+    float *__restrict__ dvec, bf16 *__restrict__ qt, bf16 *__restrict__ dot) {
   __shared__ bf16 tq[kRows][D + 2];
   __shared__ bf16 tdo[kRows][D + 2];
   const int tid = threadIdx.x;
@@ -179,13 +143,6 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(
         acc += __shfl_xor(acc, 4);
         if (part == 0 && row >= lo && row < hi) dvec[(size_t)h * n_q + row] = acc;
       }
-      for (int ci = tid; ci < kRows * D / 4; ci += 256) {
-        const int r = ci / (D / 4), c4 = ci % (D / 4);
-        const int64_t row = m * kRows + r;
-        if (row >= lo && row < hi)
-          *reinterpret_cast<float4 *>(dqacc + ((size_t)row * h_q + h) * D + 4 * c4) =
-              make_float4(0.f, 0.f, 0.f, 0.f);
-      }
       __syncthreads();
       for (int e = tid; e < D * kRows; e += 256) {
         const int dd = e / kRows, r = e % kRows;
@@ -201,36 +158,6 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(
   }
 }
 
-// dQ (bf16) <- fp32 accumulator for the covered (row, head) pairs.
-template <int D>
-__global__ __launch_bounds__(256) void bwd_finalize_kernel(const libra_tile_t *__restrict__ tiles,
-                                                           int h_q, int64_t n_q, int64_t n_kv,
-                                                           const float *__restrict__ dqacc,
-                                                           bf16 *__restrict__ dq) {
-  const libra_tile_t tl = tiles[blockIdx.x / kTileSplit];
-  if (!tile_ok(tl, n_q, n_kv, h_q)) return;
-  const int64_t ra = tl.q_row, rb = tl.q_row + (tl.q_end - tl.q_begin);
-  const int nh = tl.head_end - tl.head_begin;
-  const int64_t per_row = (int64_t)nh * D / 8;       // 8-element groups per row
-  const int64_t total = (rb - ra) * per_row;
-  for (int64_t e = (int64_t)(blockIdx.x % kTileSplit) * 256 + threadIdx.x; e < total;
-       e += (int64_t)kTileSplit * 256) {
-    const int64_t row = ra + e / per_row;
-    const int64_t rem = e % per_row;
-    const int h = tl.head_begin + (int)(rem / (D / 8));
-    const int c8 = (int)(rem % (D / 8));
-    const size_t off = ((size_t)row * h_q + h) * D + 8 * c8;
-    const float4 a = *reinterpret_cast<const float4 *>(dqacc + off);
-    const float4 b = *reinterpret_cast<const float4 *>(dqacc + off + 4);
-    bf16x8 v;
-    v[0] = static_cast<bf16>(a.x); v[1] = static_cast<bf16>(a.y);
-    v[2] = static_cast<bf16>(a.z); v[3] = static_cast<bf16>(a.w);
-    v[4] = static_cast<bf16>(b.x); v[5] = static_cast<bf16>(b.y);
-    v[6] = static_cast<bf16>(b.z); v[7] = static_cast<bf16>(b.w);
-    *reinterpret_cast<bf16x8 *>(dq + off) = v;
-  }
-}
-
 __global__ __launch_bounds__(256) void zero_kernel(uint4 *__restrict__ p, int64_t n16) {
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n16;
        i += (int64_t)gridDim.x * 256)
@@ -238,64 +165,93 @@ __global__ __launch_bounds__(256) void zero_kernel(uint4 *__restrict__ p, int64_
 }
 
 // ---------------------------------------------------------------------------
+// dK / dV kernel.
 template <int D>
-struct BwdShape {
-  static constexpr int QP = D + 8;          // Q / dO tile pitch (row-major, 32 rows)
-  static constexpr int TP = kRows + 8;      // Q^T / dO^T tile pitch (D rows)
-  static constexpr int SP = kBwdBK + 8;     // dS tile pitch (32 rows x 128 keys)
-  static constexpr int KP = D + 8;          // K block pitch (128 rows), setup only
-  static constexpr int Q_EL = kRows * QP;
-  static constexpr int T_EL = D * TP;
+struct KvShape {
+  static constexpr int QC = D / 8;          // 16-byte columns of a Q / dO row
+  static constexpr int TC = kRows / 8;      // 16-byte columns of a Q^T / dO^T row (4)
+  static constexpr int Q_EL = kRows * D;
+  static constexpr int T_EL = D * kRows;
   static constexpr int STAGE_EL = 2 * Q_EL + 2 * T_EL;
-  static constexpr int S_EL = kRows * SP;
-  static constexpr int K_EL = kBwdBK * KP;
-  static constexpr int MAIN_EL = STAGE_EL + S_EL;
-  static constexpr int BF_EL = MAIN_EL > K_EL ? MAIN_EL : K_EL;
-  static constexpr size_t SMEM = BF_EL * sizeof(bf16) + 2 * kRows * sizeof(float);
-  // dQ split: D=128 -> wave w owns d-tile w over all 8 key chunks;
-  //           D=64  -> wave w owns d-tile w&1 over key chunks 4*(w>>1)..+3.
-  static constexpr int DQ_CHUNKS = D == 128 ? 8 : 4;
+  static constexpr int NQ = kRows * QC / 64 / kWaves;   // wave loads per Q (dO) tile
+  static constexpr int NT = D * TC / 64 / kWaves;       // wave loads per Q^T (dO^T) tile
+  static constexpr size_t SMEM = 2 * STAGE_EL * sizeof(bf16) + 2 * 2 * kRows * sizeof(float);
+};
+
+// Walks the steps (32-row query block x query head) that attend one KV block:
+// tiles in list order, query blocks in row order, heads in order.
+struct StepIter {
+  const libra_tile_t *tiles;
+  int64_t T, n_q, n_kv, key0, len;
+  int h_q, g, G, kloc0;
+  int64_t t, fra, frb, qla, m;
+  int h0, h1, h;
+  bool valid;
+
+  __device__ bool seek() {
+    for (; t < T; ++t) {
+      const libra_tile_t tl = tiles[t];
+      if (!tile_ok(tl, n_q, n_kv, h_q)) continue;
+      const int64_t pb = tl.q_begin > key0 ? tl.q_begin : key0;
+      const int64_t pe = tl.q_end < key0 + len ? tl.q_end : key0 + len;
+      if (pb >= pe) continue;
+      h0 = max(tl.head_begin, g * G);
+      h1 = min(tl.head_end, (g + 1) * G);
+      if (h0 >= h1) continue;
+      fra = tl.q_row + (pb - tl.q_begin);
+      frb = fra + (pe - pb);
+      qla = pb - key0;
+      const int64_t first = fra + (kloc0 > qla ? kloc0 - qla : 0);
+      if (first >= frb) continue;
+      m = first / kRows;
+      h = h0;
+      return true;
+    }
+    return false;
+  }
+  __device__ void start() { t = 0; valid = seek(); }
+  __device__ void next() {
+    if (++h < h1) return;
+    h = h0;
+    if (++m * kRows < frb) return;
+    ++t;
+    valid = seek();
+  }
+  __device__ int64_t lo() const { return m * kRows > fra ? m * kRows : fra; }
+  __device__ int64_t hi() const { return (m + 1) * kRows < frb ? (m + 1) * kRows : frb; }
 };
 
 template <int D>
-__global__ __launch_bounds__(kThreads, 1) void attn_bwd_kernel(
+__global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
     const bf16 *__restrict__ k, const bf16 *__restrict__ v, const bf16 *__restrict__ q,
     const bf16 *__restrict__ dout, const bf16 *__restrict__ qt, const bf16 *__restrict__ dot,
     const float *__restrict__ lse, const float *__restrict__ dvec,
     const int64_t *__restrict__ cu, const libra_tile_t *__restrict__ tiles, int64_t T,
     const BwdItem *__restrict__ items, int32_t *__restrict__ hdr, int h_q, int h_kv,
     int64_t n_q, int64_t n_kv, int64_t nq_pad, float scale, float c2,
-    float *__restrict__ dqacc, void *__restrict__ dk_out, void *__restrict__ dv_out,
-    int accumulate) {
-  using S = BwdShape<D>;
+    void *__restrict__ dk_out, void *__restrict__ dv_out, int accumulate) {
+  using S = KvShape<D>;
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
-  bf16 *Qs = smem;
-  bf16 *dOs = Qs + S::Q_EL;
-  bf16 *Qts = dOs + S::Q_EL;
-  bf16 *dOts = Qts + S::T_EL;
-  bf16 *Ss = dOts + S::T_EL;
-  bf16 *Ks = smem;                                   // aliases the above during setup
-  float *lse2s = reinterpret_cast<float *>(smem + S::BF_EL);
-  float *dvs = lse2s + kRows;
+  float *fsm = reinterpret_cast<float *>(smem + 2 * S::STAGE_EL);   // [buf][lse2 | D][32]
   __shared__ int32_t s_item;
 
-  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, ln = l & 31, kg = l >> 5;
+  const int tid = threadIdx.x, l = tid & 63, ln = l & 31, kg = l >> 5;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
   const int G = h_q / h_kv;
-  const int n_items = hdr[kBwdItems];
-  const int dq_dt = D == 128 ? w : (w & 1);
-  const int dq_c0 = D == 128 ? 0 : 4 * (w >> 1);
+  int q_serve = blockIdx.x % kXcds, q_left = kXcds;
 
   for (;;) {
-    if (tid == 0) s_item = atomicAdd(&hdr[kBwdQueue], 1);
+    if (tid == 0) s_item = take_item(hdr, kBwdQ, q_serve, q_left);
     __syncthreads();
-    const int idx = s_item;
-    if (idx >= n_items) break;
-    const BwdItem it = items[idx];
-    const int64_t key0 = cu[it.sample];
-    const int64_t len = cu[it.sample + 1] - key0;
-    const int g = it.g;
-    const int kloc0 = it.kb * kBwdBK;                 // first key of the block (sample-local)
-    const int kl = kloc0 + 32 * w + ln;               // this lane's key
+    const int idx = __builtin_amdgcn_readfirstlane(s_item);
+    if (idx < 0) break;
+    const BwdItem item = items[idx];
+    const int64_t key0 = cu[item.sample];
+    const int64_t len = cu[item.sample + 1] - key0;
+    const int g = item.g;
+    const int kloc0 = item.kb * kBwdBK;
+    const int kw0 = kloc0 + 32 * w;                   // first key of this wave
+    const int kl = kw0 + ln;                          // this lane's key (sample-local)
     const bool key_ok = kl < len;
     const int64_t krow = key0 + kl;
 
@@ -310,136 +266,130 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_kernel(
 #pragma unroll
         for (int i = 0; i < 8; ++i) { kf[c][i] = bf16(0.f); vf[c][i] = bf16(0.f); }
       }
-      *reinterpret_cast<bf16x8 *>(Ks + (32 * w + ln) * S::KP + 16 * c + 8 * kg) = kf[c];
     }
-    __syncthreads();
-    // K fragments for dQ = dS K: B operand, lane = d column, 8 consecutive keys.
-    bf16x8 kq[S::DQ_CHUNKS];
-#pragma unroll
-    for (int c = 0; c < S::DQ_CHUNKS; ++c)
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        kq[c][i] = Ks[(16 * (dq_c0 + c) + 8 * kg + i) * S::KP + 32 * dq_dt + ln];
-    __syncthreads();
-
     f32x16 dva[D / 32], dka[D / 32];
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) { dva[dt][r] = 0.f; dka[dt][r] = 0.f; }
 
-    for (int64_t t = 0; t < T; ++t) {
-      const libra_tile_t tl = tiles[t];
-      if (!tile_ok(tl, n_q, n_kv, h_q)) continue;
-      const int64_t pb = tl.q_begin > key0 ? tl.q_begin : key0;
-      const int64_t pe = tl.q_end < key0 + len ? tl.q_end : key0 + len;
-      if (pb >= pe) continue;
-      const int h0 = max(tl.head_begin, g * G), h1 = min(tl.head_end, (g + 1) * G);
-      if (h0 >= h1) continue;
-      const int64_t fra = tl.q_row + (pb - tl.q_begin);   // fragment rows [fra, frb)
-      const int64_t frb = fra + (pe - pb);
-      const int64_t qla = pb - key0;                      // sample-local position of fra
-      const int64_t first = fra + (kloc0 > qla ? kloc0 - qla : 0);
-      if (first >= frb) continue;
-      for (int64_t m = first / kRows; m * kRows < frb; ++m) {
-        const int64_t lo = m * kRows > fra ? m * kRows : fra;
-        const int64_t hi = (m + 1) * kRows < frb ? (m + 1) * kRows : frb;
-        for (int h = h0; h < h1; ++h) {
-          // ---- stage the 32-row query block of head h
-          for (int ci = tid; ci < kRows * D / 8; ci += kThreads) {
-            const int r = ci / (D / 8), c8 = ci % (D / 8);
-            const int64_t row = m * kRows + r;
-            uint4 a = make_uint4(0, 0, 0, 0), b = a;
-            if (row >= lo && row < hi) {
-              const size_t off = ((size_t)row * h_q + h) * D + 8 * c8;
-              a = *reinterpret_cast<const uint4 *>(q + off);
-              b = *reinterpret_cast<const uint4 *>(dout + off);
-            }
-            *reinterpret_cast<uint4 *>(Qs + r * S::QP + 8 * c8) = a;
-            *reinterpret_cast<uint4 *>(dOs + r * S::QP + 8 * c8) = b;
-          }
-          for (int ci = tid; ci < D * kRows / 8; ci += kThreads) {
-            const int dd = ci / (kRows / 8), c8 = ci % (kRows / 8);
-            const int64_t row0 = m * kRows + 8 * c8;
-            const size_t off = ((size_t)h * D + dd) * nq_pad + row0;
-            bf16x8 a = *reinterpret_cast<const bf16x8 *>(qt + off);
-            bf16x8 b = *reinterpret_cast<const bf16x8 *>(dot + off);
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-              const bool ok = row0 + i >= lo && row0 + i < hi;
-              a[i] = ok ? a[i] : bf16(0.f);
-              b[i] = ok ? b[i] : bf16(0.f);
-            }
-            *reinterpret_cast<bf16x8 *>(Qts + dd * S::TP + 8 * c8) = a;
-            *reinterpret_cast<bf16x8 *>(dOts + dd * S::TP + 8 * c8) = b;
-          }
-          if (tid < kRows) {
-            const int64_t row = m * kRows + tid;
-            const bool ok = row >= lo && row < hi;
-            lse2s[tid] = ok ? lse[(size_t)h * n_q + row] * kLog2e : 0.f;
-            dvs[tid] = ok ? dvec[(size_t)h * n_q + row] : 0.f;
-          }
-          __syncthreads();
-
-          // ---- S = Q K^T and dP = dO V^T, queries on M (lane = key)
-          f32x16 sa, pa;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) { sa[r] = 0.f; pa[r] = 0.f; }
-          {
-            const bf16 *qp = Qs + perm32(ln) * S::QP + 8 * kg;
-            const bf16 *op = dOs + perm32(ln) * S::QP + 8 * kg;
-#pragma unroll
-            for (int c = 0; c < D / 16; ++c) {
-              sa = mfma32(*reinterpret_cast<const bf16x8 *>(qp + 16 * c), kf[c], sa);
-              pa = mfma32(*reinterpret_cast<const bf16x8 *>(op + 16 * c), vf[c], pa);
-            }
-          }
-          bf16x8 pb16[2], db16[2];
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int iq = 16 * (r >> 3) + 8 * kg + (r & 7);
-            const int64_t row = m * kRows + iq;
-            const int64_t qloc = qla + (row - fra);
-            const bool ok = key_ok && row >= lo && row < hi && kl <= qloc;
-            const float p = ok ? fast_exp2(sa[r] * c2 - lse2s[iq]) : 0.f;
-            const float ds = ok ? p * (pa[r] - dvs[iq]) : 0.f;
-            pb16[r >> 3][r & 7] = static_cast<bf16>(p);
-            db16[r >> 3][r & 7] = static_cast<bf16>(ds);
-            Ss[iq * S::SP + 32 * w + ln] = static_cast<bf16>(ds);
-          }
-          // ---- dV^T += dO^T P, dK^T += Q^T dS (d on M, keys on N, queries on K)
-#pragma unroll
-          for (int dt = 0; dt < D / 32; ++dt) {
-            const bf16 *ap = dOts + (32 * dt + perm32(ln)) * S::TP + 8 * kg;
-            const bf16 *bp = Qts + (32 * dt + perm32(ln)) * S::TP + 8 * kg;
-#pragma unroll
-            for (int c = 0; c < 2; ++c) {
-              dva[dt] = mfma32(*reinterpret_cast<const bf16x8 *>(ap + 16 * c), pb16[c], dva[dt]);
-              dka[dt] = mfma32(*reinterpret_cast<const bf16x8 *>(bp + 16 * c), db16[c], dka[dt]);
-            }
-          }
-          __syncthreads();
-          // ---- dQ = dS K over the 128 keys of the block
-          f32x16 qa;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) qa[r] = 0.f;
-          {
-            const bf16 *sp = Ss + perm32(ln) * S::SP + 8 * kg;
-#pragma unroll
-            for (int c = 0; c < S::DQ_CHUNKS; ++c)
-              qa = mfma32(*reinterpret_cast<const bf16x8 *>(sp + 16 * (dq_c0 + c)), kq[c], qa);
-          }
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int iq = 16 * (r >> 3) + 8 * kg + (r & 7);
-            const int64_t row = m * kRows + iq;
-            if (row >= lo && row < hi)
-              unsafeAtomicAdd(dqacc + ((size_t)row * h_q + h) * D + 32 * dq_dt + ln,
-                              qa[r] * scale);
-          }
-          __syncthreads();
-        }
+    // ---- staging of one step: Q, dO, Q^T, dO^T go global -> LDS directly
+    // (rows of the 32-row block outside the fragment are masked in the
+    // compute; Q^T / dO^T hold zeros there), LSE and D through registers.
+    float rl = 0.f, rd = 0.f;
+    auto issue = [&](const StepIter &st, int buf) {
+      const int64_t m0 = st.m * kRows;
+      bf16 *Qs = smem + buf * S::STAGE_EL;
+      bf16 *dOs = Qs + S::Q_EL;
+      bf16 *Qts = dOs + S::Q_EL;
+      bf16 *dOts = Qts + S::T_EL;
+      static_for<S::NQ>([&](auto u) {
+        const int wl = w + kWaves * u;
+        const int r = wl * (64 / S::QC) + l / S::QC;
+        const int col = swz<S::QC>(r, l % S::QC);
+        int64_t row = m0 + r;
+        row = row < n_q ? row : n_q - 1;
+        const size_t off = ((size_t)row * h_q + st.h) * D + 8 * col;
+        g2l16(q + off, Qs + wl * 512);
+        g2l16(dout + off, dOs + wl * 512);
+      });
+      static_for<S::NT>([&](auto u) {
+        const int wl = w + kWaves * u;
+        const int r = wl * (64 / S::TC) + l / S::TC;
+        const int col = swz<S::TC>(r, l % S::TC);
+        const size_t off = ((size_t)st.h * D + r) * nq_pad + m0 + 8 * col;
+        g2l16(qt + off, Qts + wl * 512);
+        g2l16(dot + off, dOts + wl * 512);
+      });
+      if (tid < kRows) {
+        const int lo_l = (int)(st.lo() - m0), hi_l = (int)(st.hi() - m0);
+        const bool ok = tid >= lo_l && tid < hi_l;
+        rl = ok ? lse[(size_t)st.h * n_q + m0 + tid] * kLog2e : 0.f;
+        rd = ok ? dvec[(size_t)st.h * n_q + m0 + tid] : 0.f;
       }
+    };
+    auto stash_f = [&](int buf) {
+      if (tid < kRows) {
+        fsm[buf * 2 * kRows + tid] = rl;
+        fsm[buf * 2 * kRows + kRows + tid] = rd;
+      }
+    };
+    // per-lane LDS offsets (elements) of the operand reads
+    const int prow = perm32(ln);
+    int qoff[D / 16], toff[2];
+    static_for<D / 16>([&](auto c) { qoff[c] = prow * D + 8 * swz<S::QC>(prow, 2 * c + kg); });
+    static_for<2>([&](auto c) { toff[c] = prow * kRows + 8 * swz<S::TC>(prow, 2 * c + kg); });
+
+    StepIter cur{tiles, T, n_q, n_kv, key0, len, h_q, g, G, kloc0};
+    cur.start();
+    if (cur.valid) {
+      issue(cur, 0);
+      stash_f(0);
+    }
+    wait_vm();
+    __syncthreads();
+    int buf = 0;
+    while (cur.valid) {
+      StepIter nxt = cur;
+      nxt.next();
+      if (nxt.valid) issue(nxt, buf ^ 1);
+      // ---- compute the current step from LDS buffer `buf`
+      // rows of the block are m0 + iq, iq in [0, 32); row iq is valid for this
+      // lane's key when lower <= iq < upper (inside the fragment and causal).
+      const int64_t m0 = cur.m * kRows;
+      const int lo_l = (int)(cur.lo() - m0), hi_l = (int)(cur.hi() - m0);
+      const int64_t qbase = cur.qla + (m0 - cur.fra);         // q_loc of row m0
+      const int64_t need = (int64_t)kl - qbase;               // first iq with q_loc >= kl
+      const int lower = (int)(need > lo_l ? (need < kRows ? need : kRows) : lo_l);
+      const int upper = key_ok ? hi_l : 0;
+      if ((int64_t)kw0 <= qbase + hi_l - 1) {
+        const bf16 *Qs = smem + buf * S::STAGE_EL;
+        const bf16 *dOs = Qs + S::Q_EL;
+        const bf16 *Qts = dOs + S::Q_EL;
+        const bf16 *dOts = Qts + S::T_EL;
+        const float *l2s = fsm + buf * 2 * kRows;
+        const float *dvs = l2s + kRows;
+        f32x16 sa, pa;
+        static_for<16>([&](auto r) { sa[int(r)] = 0.f; pa[int(r)] = 0.f; });
+        static_for<D / 16>([&](auto c) {
+          sa = mfma32(*reinterpret_cast<const bf16x8 *>(Qs + qoff[c]), kf[c], sa);
+          pa = mfma32(*reinterpret_cast<const bf16x8 *>(dOs + qoff[c]), vf[c], pa);
+        });
+        bf16x8 pb16[2], db16[2];
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const int iq0 = 16 * hh + 8 * kg;
+          const f32x4 la = *reinterpret_cast<const f32x4 *>(l2s + iq0);
+          const f32x4 lb = *reinterpret_cast<const f32x4 *>(l2s + iq0 + 4);
+          const f32x4 da = *reinterpret_cast<const f32x4 *>(dvs + iq0);
+          const f32x4 db = *reinterpret_cast<const f32x4 *>(dvs + iq0 + 4);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const int r = 8 * hh + i;
+            const int iq = iq0 + i;
+            const bool ok = iq >= lower && iq < upper;
+            const float l2 = i < 4 ? la[i] : lb[i - 4];
+            const float dd = i < 4 ? da[i] : db[i - 4];
+            const float p = ok ? fast_exp2(sa[r] * c2 - l2) : 0.f;
+            const float ds = ok ? p * (pa[r] - dd) : 0.f;
+            pb16[hh][i] = static_cast<bf16>(p);
+            db16[hh][i] = static_cast<bf16>(ds);
+          }
+        }
+        static_for<D / 32>([&](auto dt) {
+          const bf16 *ap = dOts + 32 * dt * kRows;
+          const bf16 *bp = Qts + 32 * dt * kRows;
+          static_for<2>([&](auto c) {
+            dva[dt] = mfma32(*reinterpret_cast<const bf16x8 *>(ap + toff[c]), pb16[c], dva[dt]);
+            dka[dt] = mfma32(*reinterpret_cast<const bf16x8 *>(bp + toff[c]), db16[c], dka[dt]);
+          });
+        });
+      }
+      if (nxt.valid) stash_f(buf ^ 1);
+      wait_vm();
+      __syncthreads();
+      buf ^= 1;
+      cur = nxt;
     }
 
     // ---- write dK, dV for this wave's 32 keys
@@ -451,12 +401,17 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_kernel(
         for (int hh = 0; hh < 2; ++hh) {
           const size_t off = base + 32 * dt + 16 * hh;
           if (accumulate) {
-            float *dkp = static_cast<float *>(dk_out) + off;
-            float *dvp = static_cast<float *>(dv_out) + off;
+            float4 *dkp = reinterpret_cast<float4 *>(static_cast<float *>(dk_out) + off);
+            float4 *dvp = reinterpret_cast<float4 *>(static_cast<float *>(dv_out) + off);
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-              dkp[i] += dka[dt][8 * hh + i] * scale;
-              dvp[i] += dva[dt][8 * hh + i];
+            for (int e = 0; e < 2; ++e) {
+              float4 a = dkp[e], b = dvp[e];
+              a.x += dka[dt][8 * hh + 4 * e + 0] * scale; b.x += dva[dt][8 * hh + 4 * e + 0];
+              a.y += dka[dt][8 * hh + 4 * e + 1] * scale; b.y += dva[dt][8 * hh + 4 * e + 1];
+              a.z += dka[dt][8 * hh + 4 * e + 2] * scale; b.z += dva[dt][8 * hh + 4 * e + 2];
+              a.w += dka[dt][8 * hh + 4 * e + 3] * scale; b.w += dva[dt][8 * hh + 4 * e + 3];
+              dkp[e] = a;
+              dvp[e] = b;
             }
           } else {
             bf16x8 a, b;
@@ -470,7 +425,164 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_kernel(
           }
         }
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dQ kernel (query-stationary; work items are the forward's).
+template <int D>
+struct DqShape {
+  static constexpr int KC = D / 8;            // 16-byte columns of a K / V row
+  static constexpr int TC = kFwdBN / 8;       // 16-byte columns of a K^T row
+  static constexpr int K_EL = kFwdBN * D;
+  static constexpr int T_EL = D * kFwdBN;
+  static constexpr int STAGE = 2 * K_EL + T_EL;
+  static constexpr int NK = kFwdBN * KC / 64 / kWaves;
+  static constexpr int NT = D * TC / 64 / kWaves;
+  static constexpr size_t SMEM = 2 * STAGE * sizeof(bf16);
+};
+
+template <int D>
+__global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
+    const bf16 *__restrict__ q, const bf16 *__restrict__ dout, const bf16 *__restrict__ k,
+    const bf16 *__restrict__ v, const bf16 *__restrict__ kt, const float *__restrict__ lse,
+    const float *__restrict__ dvec, const int64_t *__restrict__ cu,
+    const FwdItem *__restrict__ items, int32_t *__restrict__ hdr, int h_q, int h_kv,
+    int64_t n_q, int64_t n_kv, int64_t pitch, float c2, float scale, bf16 *__restrict__ dq) {
+  using S = DqShape<D>;
+  extern __shared__ __attribute__((aligned(16))) bf16 smem[];
+  __shared__ int32_t s_item;
+  const int tid = threadIdx.x, l = tid & 63, ln = l & 31, kg = l >> 5;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
+  int q_serve = blockIdx.x % kXcds, q_left = kXcds;
+  const int prow = perm32(ln);
+  int koff[D / 16], toff_l[4];
+  static_for<D / 16>([&](auto c) { koff[c] = prow * D + 8 * swz<S::KC>(prow, 2 * c + kg); });
+  static_for<4>([&](auto c) { toff_l[c] = prow * kFwdBN + 8 * swz<S::TC>(prow, 2 * c + kg); });
+
+  for (;;) {
+    if (tid == 0) s_item = take_item(hdr, kFwdQ, q_serve, q_left);
     __syncthreads();
+    const int idx = __builtin_amdgcn_readfirstlane(s_item);
+    if (idx < 0) break;
+    const FwdItem it = items[idx];
+    const int64_t key0 = cu[it.sample];
+    const int64_t toff = vt_offset(key0, it.sample);
+    const int head = it.head0 + (w % it.nh);
+    const int wrow0 = (w / it.nh) * kRows;
+    const int wrows = min(max(it.nrows - wrow0, 0), kRows);
+    const bool active = wrows > 0;
+    const int my_r = active ? min(ln, wrows - 1) : 0;
+    const int64_t row = (int64_t)it.q_row0 + wrow0 + my_r;
+    const int qloc = it.q_loc0 + wrow0 + my_r;
+    const int wave_qmin = it.q_loc0 + wrow0;
+    const int nkb = (it.q_loc0 + it.nrows - 1) / kFwdBN + 1;
+    const int wave_nkb = active ? (it.q_loc0 + wrow0 + wrows - 1) / kFwdBN + 1 : 0;
+
+    bf16x8 qf[D / 16], of[D / 16];
+    float l2 = 0.f, dd_q = 0.f;
+    if (active) {
+      const size_t off = ((size_t)row * h_q + head) * D + 8 * kg;
+#pragma unroll
+      for (int c = 0; c < D / 16; ++c) {
+        qf[c] = *reinterpret_cast<const bf16x8 *>(q + off + 16 * c);
+        of[c] = *reinterpret_cast<const bf16x8 *>(dout + off + 16 * c);
+      }
+      l2 = lse[(size_t)head * n_q + row] * kLog2e;
+      dd_q = dvec[(size_t)head * n_q + row];
+    }
+    f32x16 acc[D / 32];
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[dt][r] = 0.f;
+
+    // global -> LDS, asynchronous: K and V rows of block b (keys past the
+    // buffer read the last key instead; they are masked) and the K^T block
+    // of the padded transposed copy
+    auto issue = [&](int b, int buf) {
+      bf16 *Ks = smem + buf * S::STAGE;
+      bf16 *Vs = Ks + S::K_EL;
+      bf16 *Ts = Vs + S::K_EL;
+      static_for<S::NK>([&](auto u) {
+        const int wl = w + kWaves * u;
+        const int r = wl * (64 / S::KC) + l / S::KC;
+        const int col = swz<S::KC>(r, l % S::KC);
+        int64_t key = key0 + (int64_t)b * kFwdBN + r;
+        key = key < n_kv ? key : n_kv - 1;
+        const size_t off = ((size_t)key * h_kv + it.g) * D + 8 * col;
+        g2l16(k + off, Ks + wl * 512);
+        g2l16(v + off, Vs + wl * 512);
+      });
+      static_for<S::NT>([&](auto u) {
+        const int wl = w + kWaves * u;
+        const int r = wl * (64 / S::TC) + l / S::TC;
+        const int col = swz<S::TC>(r, l % S::TC);
+        g2l16(kt + ((size_t)it.g * D + r) * pitch + toff + (int64_t)b * kFwdBN + 8 * col,
+              Ts + wl * 512);
+      });
+    };
+
+    issue(0, 0);
+    wait_vm();
+    __syncthreads();
+    for (int b = 0; b < nkb; ++b) {
+      const int buf = b & 1;
+      if (b + 1 < nkb) issue(b + 1, buf ^ 1);
+      if (b < wave_nkb) {
+        const bf16 *Ks = smem + buf * S::STAGE;
+        const bf16 *Vs = Ks + S::K_EL;
+        const bf16 *Ts = Vs + S::K_EL;
+        f32x16 s[2], dp[2];
+        static_for<2>([&](auto t) {
+          static_for<16>([&](auto r) { s[t][int(r)] = 0.f; dp[t][int(r)] = 0.f; });
+          static_for<D / 16>([&](auto c) {
+            s[t] = mfma32(*reinterpret_cast<const bf16x8 *>(Ks + 32 * t * D + koff[c]), qf[c],
+                          s[t]);
+            dp[t] = mfma32(*reinterpret_cast<const bf16x8 *>(Vs + 32 * t * D + koff[c]), of[c],
+                           dp[t]);
+          });
+        });
+        // causal mask only in blocks that reach past the wave's first row
+        if (b * kFwdBN + kFwdBN - 1 > wave_qmin) {
+          static_for<2>([&](auto t) {
+            static_for<16>([&](auto r) {
+              const int kl = b * kFwdBN + 32 * t + 16 * (r >> 3) + 8 * kg + (r & 7);
+              if (kl > qloc) s[t][int(r)] = -INFINITY;
+            });
+          });
+        }
+        bf16x8 dsf[4];
+        const float neg_l2 = -l2;
+        static_for<2>([&](auto t) {
+          static_for<16>([&](auto r) {
+            const float p = fast_exp2(__builtin_fmaf(s[t][int(r)], c2, neg_l2));
+            dsf[2 * t + (r >> 3)][r & 7] = static_cast<bf16>(p * (dp[t][int(r)] - dd_q));
+          });
+        });
+        static_for<D / 32>([&](auto dt) {
+          static_for<4>([&](auto c) {
+            acc[dt] = mfma32(*reinterpret_cast<const bf16x8 *>(Ts + 32 * dt * kFwdBN + toff_l[c]),
+                             dsf[c], acc[dt]);
+          });
+        });
+      }
+      wait_vm();
+      __syncthreads();
+    }
+
+    if (active && ln < wrows) {
+      bf16 *op = dq + ((size_t)row * h_q + head) * D + 8 * kg;
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          bf16x8 ov;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) ov[i] = static_cast<bf16>(acc[dt][8 * hh + i] * scale);
+          *reinterpret_cast<bf16x8 *>(op + 32 * dt + 16 * hh) = ov;
+        }
+    }
   }
 }
 
@@ -478,19 +590,21 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_kernel(
 static size_t align256b(size_t x) { return (x + 255) / 256 * 256; }
 
 BwdLayout bwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, int h_kv, int d) {
-  (void)T;
   BwdLayout L;
   L.max_items = (n_kv / kBwdBK + n + 1) * (int64_t)h_kv;
+  L.max_qitems = fwd_max_items(T, n, n_q, h_q, h_kv);
   L.nq_pad = (n_q + kRows - 1) / kRows * kRows;
+  L.pitch = vt_pitch(n_kv, n);
   L.hdr = 0;
   L.ext = align256b(kHdrSlots * sizeof(int32_t));
   L.gmask = align256b(L.ext + (size_t)n * sizeof(int32_t));
   L.items = align256b(L.gmask + (size_t)n * sizeof(unsigned long long));
-  L.dvec = align256b(L.items + (size_t)L.max_items * sizeof(BwdItem));
+  L.qitems = align256b(L.items + (size_t)L.max_items * sizeof(BwdItem));
+  L.dvec = align256b(L.qitems + (size_t)L.max_qitems * sizeof(FwdItem));
   L.qt = align256b(L.dvec + (size_t)h_q * n_q * sizeof(float));
   L.dot = align256b(L.qt + (size_t)h_q * d * L.nq_pad * sizeof(bf16));
-  L.dqacc = align256b(L.dot + (size_t)h_q * d * L.nq_pad * sizeof(bf16));
-  L.total = align256b(L.dqacc + (size_t)n_q * h_q * d * sizeof(float));
+  L.kt = align256b(L.dot + (size_t)h_q * d * L.nq_pad * sizeof(bf16));
+  L.total = align256b(L.kt + (size_t)h_kv * d * L.pitch * sizeof(bf16));
   return L;
 }
 
@@ -499,20 +613,25 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
                         const float *lse, const bf16 *dout, const int64_t *cu, int64_t n,
                         const libra_tile_t *tiles, int64_t T, int64_t n_q, int64_t n_kv, int h_q,
                         int h_kv, float scale, bf16 *dq, void *dk, void *dv, bool accumulate,
-                        char *ws, const BwdLayout &L, hipStream_t st, const KernelTimer *tm) {
+                        char *ws, const BwdLayout &L, hipStream_t st, const KernelTimer *tm_kv,
+                        const KernelTimer *tm_q) {
   int32_t *hdr = reinterpret_cast<int32_t *>(ws + L.hdr);
   int32_t *ext = reinterpret_cast<int32_t *>(ws + L.ext);
   auto *gmask = reinterpret_cast<unsigned long long *>(ws + L.gmask);
   BwdItem *items = reinterpret_cast<BwdItem *>(ws + L.items);
+  FwdItem *qitems = reinterpret_cast<FwdItem *>(ws + L.qitems);
   float *dvec = reinterpret_cast<float *>(ws + L.dvec);
   bf16 *qt = reinterpret_cast<bf16 *>(ws + L.qt);
   bf16 *dot = reinterpret_cast<bf16 *>(ws + L.dot);
-  float *dqacc = reinterpret_cast<float *>(ws + L.dqacc);
+  bf16 *kt = reinterpret_cast<bf16 *>(ws + L.kt);
   static bool attr_set = false;
   if (!attr_set) {
-    if (hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_bwd_kernel<D>),
+    if (hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_bwd_dkdv_kernel<D>),
                             hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)BwdShape<D>::SMEM) != hipSuccess)
+                            (int)KvShape<D>::SMEM) != hipSuccess ||
+        hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_bwd_dq_kernel<D>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)DqShape<D>::SMEM) != hipSuccess)
       return fail(LIBRA_EHIP, "hipFuncSetAttribute failed");
     attr_set = true;
   }
@@ -525,18 +644,33 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
   if (T > 0) {
     hipLaunchKernelGGL(prep_bwd_kernel, dim3(1), dim3(kPrepThreads), 0, st, cu, n, tiles, T, h_q,
                        h_kv, n_q, n_kv, hdr, ext, gmask, items, L.max_items);
+    enqueue_fwd_items(cu, n, tiles, T, h_q, h_kv, n_q, n_kv, hdr, qitems, L.max_qitems, st);
+    {
+      // Q^T / dO^T are zero outside the covered rows: query blocks of the
+      // dK/dV kernel contract over all 32 rows of a block
+      const int64_t n16 = (int64_t)h_q * D * L.nq_pad * (int64_t)sizeof(bf16) / 16;
+      const unsigned blocks = (unsigned)std::min<int64_t>((n16 + 255) / 256, 4096);
+      hipLaunchKernelGGL(zero_kernel, dim3(blocks), dim3(256), 0, st, reinterpret_cast<uint4 *>(qt),
+                         n16);
+      hipLaunchKernelGGL(zero_kernel, dim3(blocks), dim3(256), 0, st,
+                         reinterpret_cast<uint4 *>(dot), n16);
+    }
     hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)(T * kTileSplit)), dim3(256), 0, st, q, o,
-                       dout, tiles, h_q, n_q, n_kv, L.nq_pad, dvec, qt, dot, dqacc);
+                       dout, tiles, h_q, n_q, n_kv, L.nq_pad, dvec, qt, dot);
+    enqueue_transpose(k, cu, n, n_kv, h_kv, D, L.pitch, kt, st);
     int dev = 0, cus = 256;
     hipGetDevice(&dev);
     hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (tm) hipEventRecord(tm->begin, st);
-    hipLaunchKernelGGL(attn_bwd_kernel<D>, dim3(cus), dim3(kThreads), BwdShape<D>::SMEM, st, k, v,
-                       q, dout, qt, dot, lse, dvec, cu, tiles, T, items, hdr, h_q, h_kv, n_q, n_kv,
-                       L.nq_pad, scale, scale * kLog2e, dqacc, dk, dv, accumulate ? 1 : 0);
-    if (tm) hipEventRecord(tm->end, st);
-    hipLaunchKernelGGL(bwd_finalize_kernel<D>, dim3((unsigned)(T * kTileSplit)), dim3(256), 0, st,
-                       tiles, h_q, n_q, n_kv, dqacc, dq);
+    if (tm_kv) hipEventRecord(tm_kv->begin, st);
+    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(cus), dim3(kThreads), KvShape<D>::SMEM, st, k,
+                       v, q, dout, qt, dot, lse, dvec, cu, tiles, T, items, hdr, h_q, h_kv, n_q,
+                       n_kv, L.nq_pad, scale, scale * kLog2e, dk, dv, accumulate ? 1 : 0);
+    if (tm_kv) hipEventRecord(tm_kv->end, st);
+    if (tm_q) hipEventRecord(tm_q->begin, st);
+    hipLaunchKernelGGL(attn_bwd_dq_kernel<D>, dim3(cus), dim3(kThreads), DqShape<D>::SMEM, st, q,
+                       dout, k, v, kt, lse, dvec, cu, qitems, hdr, h_q, h_kv, n_q, n_kv, L.pitch,
+                       scale * kLog2e, scale, dq);
+    if (tm_q) hipEventRecord(tm_q->end, st);
   }
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(LIBRA_EHIP, "backward launch failed: %s", hipGetErrorString(e));
@@ -547,7 +681,7 @@ int launch_bwd(const void *q, const void *k, const void *v, const void *o, const
                const void *dout, const int64_t *cu, int64_t n, const libra_tile_t *tiles,
                int64_t T, int64_t n_q, int64_t n_kv, int h_q, int h_kv, int d, float scale,
                void *dq, void *dk, void *dv, bool accumulate, void *ws, const BwdLayout &L,
-               hipStream_t st, const KernelTimer *tm) {
+               hipStream_t st, const KernelTimer *tm_kv, const KernelTimer *tm_q) {
   auto Q = static_cast<const bf16 *>(q);
   auto K = static_cast<const bf16 *>(k);
   auto V = static_cast<const bf16 *>(v);
@@ -557,9 +691,9 @@ int launch_bwd(const void *q, const void *k, const void *v, const void *o, const
   char *W = static_cast<char *>(ws);
   if (d == 128)
     return launch_bwd_d<128>(Q, K, V, O, lse, dO, cu, n, tiles, T, n_q, n_kv, h_q, h_kv, scale,
-                             dQ, dk, dv, accumulate, W, L, st, tm);
+                             dQ, dk, dv, accumulate, W, L, st, tm_kv, tm_q);
   return launch_bwd_d<64>(Q, K, V, O, lse, dO, cu, n, tiles, T, n_q, n_kv, h_q, h_kv, scale, dQ,
-                          dk, dv, accumulate, W, L, st, tm);
+                          dk, dv, accumulate, W, L, st, tm_kv, tm_q);
 }
 
 }  // namespace libra

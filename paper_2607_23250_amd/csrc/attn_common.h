@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 #include "libra.h"
 
@@ -24,19 +25,93 @@ constexpr int kRows = 32;
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 
-// Buckets of the longest-first ordering of work items.
-constexpr int kBuckets = 8192;
+// Work items are ordered longest-first in one queue per XCD (8 XCDs of 32
+// CUs, each with its own L2): items that stream the same K/V (forward, dQ) or
+// the same query blocks (dK/dV) share a queue, so the CUs of one XCD read the
+// same blocks at about the same time.  A workgroup serves the queue of its XCD
+// (workgroups are dispatched round-robin over the XCDs) and moves on to the
+// other queues when it runs dry.
+constexpr int kXcds = 8;
+constexpr int kQBuckets = 1024;      // cost buckets per queue
 constexpr int kPrepThreads = 1024;
 
-// Workspace header (int32 slots).
+// Workspace header (int32 slots).  A queue set at `base` keeps the queue
+// heads at [base, base+8), item counts at [base+8, base+16) and segment
+// starts at [base+16, base+24).
 enum HdrSlot {
-  kFwdQueue = 0,   // next forward item to take
-  kFwdItems = 1,   // number of forward items
-  kBwdQueue = 2,
-  kBwdItems = 3,
-  kBadTiles = 4,   // tiles skipped because they were out of range
+  kBadTiles = 4,   // tiles skipped because they were out of range (+1 on item overflow)
+  kFwdQ = 8,       // forward / dQ work items
+  kBwdQ = 32,      // dK/dV work items
   kHdrSlots = 64
 };
+
+// Cost bucket, 0 = longest: exact below 512, then 32 units per bucket.
+__device__ __forceinline__ int cost_bucket(int64_t c) {
+  const int64_t b = c < 512 ? c : 512 + (c - 512) / 32;
+  return kQBuckets - 1 - (int)(b < kQBuckets - 1 ? b : kQBuckets - 1);
+}
+
+// One workgroup of kPrepThreads: counts items per (queue, bucket), scans, and
+// scatters them so that each queue's segment is longest-first.  `each(f)`
+// must call f(item, cost, queue) once per item, in the same way every time.
+template <typename Item, typename Each>
+__device__ void build_queues(Each &&each, int32_t *hist, int32_t *part, int32_t *hdr, int base,
+                             Item *out, int64_t max_items) {
+  const int tid = threadIdx.x;
+  for (int i = tid; i < kXcds * kQBuckets; i += kPrepThreads) hist[i] = 0;
+  __syncthreads();
+  each([&](const Item &, int64_t cost, int x) {
+    atomicAdd(&hist[x * kQBuckets + cost_bucket(cost)], 1);
+  });
+  __syncthreads();
+  constexpr int per = kXcds * kQBuckets / kPrepThreads;
+  int32_t s = 0;
+  for (int i = 0; i < per; ++i) s += hist[tid * per + i];
+  part[tid] = s;
+  __syncthreads();
+  for (int o = 1; o < kPrepThreads; o <<= 1) {
+    const int32_t v = tid >= o ? part[tid - o] : 0;
+    __syncthreads();
+    part[tid] += v;
+    __syncthreads();
+  }
+  int32_t pos = part[tid] - s;
+  constexpr int threads_per_queue = kPrepThreads / kXcds;
+  if (tid % threads_per_queue == 0) {
+    const int x = tid / threads_per_queue;
+    const int32_t start = pos;
+    const int32_t end = part[tid + threads_per_queue - 1];
+    const int32_t lim = (int32_t)(max_items < INT32_MAX ? max_items : INT32_MAX);
+    hdr[base + x] = 0;
+    hdr[base + kXcds + x] = (end < lim ? end : lim) - (start < lim ? start : lim);
+    hdr[base + 2 * kXcds + x] = start;
+    if (x == kXcds - 1 && end > lim) atomicAdd(&hdr[kBadTiles], 1);
+  }
+  __syncthreads();
+  for (int i = 0; i < per; ++i) {
+    const int32_t cnt = hist[tid * per + i];
+    hist[tid * per + i] = pos;
+    pos += cnt;
+  }
+  __syncthreads();
+  each([&](const Item &it, int64_t cost, int x) {
+    const int32_t p = atomicAdd(&hist[x * kQBuckets + cost_bucket(cost)], 1);
+    if (p < max_items) out[p] = it;
+  });
+}
+
+// Thread 0 of a persistent workgroup: index of the next item to run, or -1.
+// `q` is the queue being served (starts at the workgroup's XCD), `left` the
+// number of queues not yet found empty.
+__device__ __forceinline__ int take_item(int32_t *hdr, int base, int &q, int &left) {
+  while (left > 0) {
+    const int got = atomicAdd(&hdr[base + q], 1);
+    if (got < hdr[base + kXcds + q]) return hdr[base + 2 * kXcds + q] + got;
+    q = (q + 1) % kXcds;
+    --left;
+  }
+  return -1;
+}
 
 // One forward work item: up to 4 query heads of one KV group x up to
 // 32 * (4 / heads) consecutive rows of one sample fragment of one tile.
@@ -82,6 +157,38 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// LDS tiles are stored without padding; the 16-byte column of a row is
+// XOR-swizzled with the row index so that the 16 lanes that read 16
+// consecutive rows at the same logical column hit 16 different bank groups.
+// C = 16-byte columns per row (4, 8 or 16).
+template <int C>
+__device__ __forceinline__ int swz(int row, int col) {
+  return col ^ ((row / (16 / C)) & (C - 1));
+}
+
+// Asynchronous 16-byte global -> LDS copy by one wave: lane i's bytes land at
+// lds + 16 * i; `lds` must be the same for every lane of the wave.
+__device__ __forceinline__ void g2l16(const void *g, bf16 *lds) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void *)lds, 16, 0, 0);
+}
+// Wait for this wave's outstanding global loads (including global -> LDS).
+__device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Compile-time loop: f(std::integral_constant<int, i>{}) for i in [0, N).  Register
+// arrays indexed this way are kept in registers (a runtime-indexed or
+// captured array can end up in scratch memory).
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for_impl(F &&f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for_impl<I + 1, N>(f);
+  }
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+  static_for_impl<0, N>(f);
+}
+
 // First index i in [0, n] with a[i] > x (a sorted ascending, n+1 entries read at most n).
 __device__ __forceinline__ int64_t upper_bound64(const int64_t *a, int64_t n, int64_t x) {
   int64_t lo = 0, hi = n;
@@ -107,8 +214,9 @@ struct FwdLayout {
   int64_t max_items = 0, pitch = 0;
 };
 struct BwdLayout {
-  size_t hdr = 0, ext = 0, gmask = 0, items = 0, dvec = 0, qt = 0, dot = 0, dqacc = 0, total = 0;
-  int64_t max_items = 0, nq_pad = 0;
+  size_t hdr = 0, ext = 0, gmask = 0, items = 0, qitems = 0, dvec = 0, qt = 0, dot = 0, kt = 0,
+         total = 0;
+  int64_t max_items = 0, max_qitems = 0, nq_pad = 0, pitch = 0;
 };
 
 FwdLayout fwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, int h_kv, int d);
@@ -119,6 +227,15 @@ struct KernelTimer {
   hipEvent_t begin = nullptr, end = nullptr;
 };
 
+// Shared preparation passes (attn_fwd.hip): forward-style work items (also
+// used by the dQ kernel) and the padded transpose of K or V.
+void enqueue_fwd_items(const int64_t *cu, int64_t n, const libra_tile_t *tiles, int64_t T,
+                       int h_q, int h_kv, int64_t n_q, int64_t n_kv, int32_t *hdr,
+                       FwdItem *items, int64_t max_items, hipStream_t st);
+void enqueue_transpose(const void *src, const int64_t *cu, int64_t n, int64_t n_kv, int h_kv,
+                       int d, int64_t pitch, void *dst, hipStream_t st);
+int64_t fwd_max_items(int64_t T, int64_t n, int64_t n_q, int h_q, int h_kv);
+
 int launch_fwd(const void *q, const void *k, const void *v, const int64_t *cu, int64_t n,
                const libra_tile_t *tiles, int64_t T, int64_t n_q, int64_t n_kv, int h_q,
                int h_kv, int d, float scale, void *o, float *lse, void *ws,
@@ -127,6 +244,6 @@ int launch_bwd(const void *q, const void *k, const void *v, const void *o, const
                const void *dout, const int64_t *cu, int64_t n, const libra_tile_t *tiles,
                int64_t T, int64_t n_q, int64_t n_kv, int h_q, int h_kv, int d, float scale,
                void *dq, void *dk, void *dv, bool accumulate, void *ws, const BwdLayout &L,
-               hipStream_t st, const KernelTimer *tm);
+               hipStream_t st, const KernelTimer *tm_kv, const KernelTimer *tm_q);
 
 }  // namespace libra

@@ -54,68 +54,43 @@ __device__ void for_each_fwd_item(const libra_tile_t &t, const int64_t *cu, int6
   }
 }
 
-// One workgroup: count items per cost bucket, order buckets longest-first,
-// scatter.  Also resets the queue.  Tiles outside the buffers are skipped and
-// counted in hdr[kBadTiles].
+// One workgroup: every tile's items, longest-first, one queue per XCD keyed
+// by (KV head, head chunk) so that an XCD streams few K/V sequences.  Tiles
+// outside the buffers are skipped and counted in hdr[kBadTiles].
 __global__ __launch_bounds__(kPrepThreads) void prep_fwd_kernel(
     const int64_t *__restrict__ cu, int64_t n, const libra_tile_t *__restrict__ tiles, int64_t T,
     int h_q, int h_kv, int64_t n_q, int64_t n_kv, int32_t *__restrict__ hdr,
     FwdItem *__restrict__ items, int64_t max_items) {
-  __shared__ int32_t hist[kBuckets];
+  __shared__ int32_t hist[kXcds * kQBuckets];
   __shared__ int32_t part[kPrepThreads];
-  __shared__ int32_t bad;
   const int tid = threadIdx.x;
   const int G = h_q / h_kv;
-  for (int i = tid; i < kBuckets; i += kPrepThreads) hist[i] = 0;
-  if (tid == 0) bad = 0;
+  const int chunks = (G + 3) / 4;                    // head chunks per KV group
+  const int keys = h_kv * chunks;
+  const int R = keys >= kXcds ? 1 : kXcds / keys;    // queues per key
+  if (tid == 0) hdr[kBadTiles] = 0;
+  __threadfence();
   __syncthreads();
-  auto bucket = [](int nkb) { return kBuckets - (nkb < kBuckets ? nkb : kBuckets); };
-  for (int64_t t = tid; t < T; t += kPrepThreads) {
-    const libra_tile_t tl = tiles[t];
-    if (!tile_ok(tl, n_q, n_kv, h_q)) { atomicAdd(&bad, 1); continue; }
-    for_each_fwd_item(tl, cu, n, G, [&](const FwdItem &, int nkb) {
-      atomicAdd(&hist[bucket(nkb)], 1);
-    });
-  }
-  __syncthreads();
-  // exclusive scan over buckets (bucket 0 = longest)
-  constexpr int per = kBuckets / kPrepThreads;
-  int32_t s = 0;
-  for (int i = 0; i < per; ++i) s += hist[tid * per + i];
-  part[tid] = s;
-  __syncthreads();
-  for (int o = 1; o < kPrepThreads; o <<= 1) {
-    const int32_t v = tid >= o ? part[tid - o] : 0;
-    __syncthreads();
-    part[tid] += v;
-    __syncthreads();
-  }
-  int32_t base = part[tid] - s;
-  const int32_t total = part[kPrepThreads - 1];
-  __syncthreads();
-  for (int i = 0; i < per; ++i) {
-    const int32_t c = hist[tid * per + i];
-    hist[tid * per + i] = base;
-    base += c;
-  }
-  __syncthreads();
-  for (int64_t t = tid; t < T; t += kPrepThreads) {
-    const libra_tile_t tl = tiles[t];
-    if (!tile_ok(tl, n_q, n_kv, h_q)) continue;
-    for_each_fwd_item(tl, cu, n, G, [&](const FwdItem &it, int nkb) {
-      const int32_t pos = atomicAdd(&hist[bucket(nkb)], 1);
-      if (pos < max_items) items[pos] = it;
-    });
-  }
-  if (tid == 0) {
-    hdr[kFwdQueue] = 0;
-    hdr[kFwdItems] = total < max_items ? total : (int32_t)max_items;
-    hdr[kBadTiles] = bad + (total > max_items ? 1 : 0);
-  }
+  int bad = 0;
+  for (int64_t t = tid; t < T; t += kPrepThreads)
+    if (!tile_ok(tiles[t], n_q, n_kv, h_q)) ++bad;
+  if (bad) atomicAdd(&hdr[kBadTiles], bad);
+  auto each = [&](auto &&f) {
+    for (int64_t t = tid; t < T; t += kPrepThreads) {
+      const libra_tile_t tl = tiles[t];
+      if (!tile_ok(tl, n_q, n_kv, h_q)) continue;
+      for_each_fwd_item(tl, cu, n, G, [&](const FwdItem &it, int nkb) {
+        const int key = it.g * chunks + (it.head0 - it.g * G) / 4;
+        const int x = (key * R + (it.q_row0 / 128) % R) % kXcds;
+        f(it, (int64_t)nkb, x);
+      });
+    }
+  };
+  build_queues<FwdItem>(each, hist, part, hdr, kFwdQ, items, max_items);
 }
 
 // ---------------------------------------------------------------------------
-// V [n_kv][h_kv][D] -> Vt [h_kv][D][pitch]; sample j occupies
+// V (or K) [n_kv][h_kv][D] -> [h_kv][D][pitch]; sample j occupies
 // [vt_offset(cu[j], j), +ceil64(len)), zero padded past its length.
 template <int D>
 __global__ __launch_bounds__(256) void transpose_v_kernel(const bf16 *__restrict__ v,
@@ -164,13 +139,13 @@ __global__ __launch_bounds__(256) void transpose_v_kernel(const bf16 *__restrict
 // ---------------------------------------------------------------------------
 template <int D>
 struct FwdShape {
-  static constexpr int KP = D + 8;            // K tile pitch (elements)
-  static constexpr int VP = kFwdBN + 8;       // V^T tile pitch
-  static constexpr int K_EL = kFwdBN * KP;
-  static constexpr int V_EL = D * VP;
+  static constexpr int KC = D / 8;            // 16-byte columns of a K row
+  static constexpr int VC = kFwdBN / 8;       // 16-byte columns of a V^T row
+  static constexpr int K_EL = kFwdBN * D;
+  static constexpr int V_EL = D * kFwdBN;
   static constexpr int STAGE = K_EL + V_EL;
-  static constexpr int NK = kFwdBN * D / 8 / kThreads;   // 16-byte K loads per thread
-  static constexpr int NV = D * kFwdBN / 8 / kThreads;   // 16-byte V^T loads per thread
+  static constexpr int NK = kFwdBN * KC / 64 / kWaves;   // wave loads of 1 KB per K tile
+  static constexpr int NV = D * VC / 64 / kWaves;        // wave loads per V^T tile
   static constexpr size_t SMEM = 2 * STAGE * sizeof(bf16);
 };
 
@@ -183,14 +158,20 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
   using S = FwdShape<D>;
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
   __shared__ int32_t s_item;
-  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, ln = l & 31, kg = l >> 5;
-  const int n_items = hdr[kFwdItems];
+  const int tid = threadIdx.x, l = tid & 63, ln = l & 31, kg = l >> 5;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
+  int q_serve = blockIdx.x % kXcds, q_left = kXcds;
+  // per-lane LDS offsets (elements) of the operand reads, fixed for the kernel
+  const int prow = perm32(ln);
+  int koff[D / 16], voff_l[4];
+  static_for<D / 16>([&](auto c) { koff[c] = prow * D + 8 * swz<S::KC>(prow, 2 * c + kg); });
+  static_for<4>([&](auto c) { voff_l[c] = prow * kFwdBN + 8 * swz<S::VC>(prow, 2 * c + kg); });
 
   for (;;) {
-    if (tid == 0) s_item = atomicAdd(&hdr[kFwdQueue], 1);
+    if (tid == 0) s_item = take_item(hdr, kFwdQ, q_serve, q_left);
     __syncthreads();
-    const int idx = s_item;
-    if (idx >= n_items) break;
+    const int idx = __builtin_amdgcn_readfirstlane(s_item);
+    if (idx < 0) break;
     const FwdItem it = items[idx];
     const int64_t key0 = cu[it.sample];
     const int64_t voff = vt_offset(key0, it.sample);
@@ -208,113 +189,98 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     bf16x8 qf[D / 16];
     if (active) {
       const bf16 *qp = q + ((size_t)row * h_q + head) * D + 8 * kg;
-#pragma unroll
-      for (int c = 0; c < D / 16; ++c) qf[c] = *reinterpret_cast<const bf16x8 *>(qp + 16 * c);
+      static_for<D / 16>([&](auto c) { qf[c] = *reinterpret_cast<const bf16x8 *>(qp + 16 * c); });
     }
     f32x16 oacc[D / 32];
-#pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[dt][r] = 0.f;
+    static_for<D / 32>([&](auto dt) { static_for<16>([&](auto r) { oacc[dt][int(r)] = 0.f; }); });
     float m_run = -INFINITY, l_run = 0.f;
 
-    // staging: registers <- global for block b
-    uint4 kreg[S::NK], vreg[S::NV];
-    auto fetch = [&](int b) {
-#pragma unroll
-      for (int u = 0; u < S::NK; ++u) {
-        const int ci = tid + kThreads * u;
-        const int r = ci / (D / 8), c8 = ci % (D / 8);
-        const int64_t key = key0 + (int64_t)b * kFwdBN + r;
-        kreg[u] = key < n_kv ? *reinterpret_cast<const uint4 *>(
-                                   k + ((size_t)key * h_kv + it.g) * D + 8 * c8)
-                             : make_uint4(0, 0, 0, 0);
-      }
-#pragma unroll
-      for (int u = 0; u < S::NV; ++u) {
-        const int ci = tid + kThreads * u;
-        const int dd = ci / (kFwdBN / 8), c8 = ci % (kFwdBN / 8);
-        vreg[u] = *reinterpret_cast<const uint4 *>(
-            vt + ((size_t)it.g * D + dd) * pitch + voff + (int64_t)b * kFwdBN + 8 * c8);
-      }
-    };
-    auto stash = [&](int buf) {
+    // global -> LDS, asynchronous: K block b (keys past the buffer read the
+    // last key instead; they are masked) and the V^T block of the padded copy
+    auto issue = [&](int b, int buf) {
       bf16 *Ks = smem + buf * S::STAGE;
       bf16 *Vs = Ks + S::K_EL;
-#pragma unroll
-      for (int u = 0; u < S::NK; ++u) {
-        const int ci = tid + kThreads * u;
-        const int r = ci / (D / 8), c8 = ci % (D / 8);
-        *reinterpret_cast<uint4 *>(Ks + r * S::KP + 8 * c8) = kreg[u];
-      }
-#pragma unroll
-      for (int u = 0; u < S::NV; ++u) {
-        const int ci = tid + kThreads * u;
-        const int dd = ci / (kFwdBN / 8), c8 = ci % (kFwdBN / 8);
-        *reinterpret_cast<uint4 *>(Vs + dd * S::VP + 8 * c8) = vreg[u];
-      }
+      static_for<S::NK>([&](auto u) {
+        const int wl = w + kWaves * u;
+        const int r = wl * (64 / S::KC) + l / S::KC;
+        const int col = swz<S::KC>(r, l % S::KC);
+        int64_t key = key0 + (int64_t)b * kFwdBN + r;
+        key = key < n_kv ? key : n_kv - 1;
+        g2l16(k + ((size_t)key * h_kv + it.g) * D + 8 * col, Ks + wl * 512);
+      });
+      static_for<S::NV>([&](auto u) {
+        const int wl = w + kWaves * u;
+        const int r = wl * (64 / S::VC) + l / S::VC;
+        const int col = swz<S::VC>(r, l % S::VC);
+        g2l16(vt + ((size_t)it.g * D + r) * pitch + voff + (int64_t)b * kFwdBN + 8 * col,
+              Vs + wl * 512);
+      });
     };
 
-    fetch(0);
-    stash(0);
+    issue(0, 0);
+    wait_vm();
     __syncthreads();
     for (int b = 0; b < nkb; ++b) {
       const int buf = b & 1;
-      if (b + 1 < nkb) fetch(b + 1);
+      if (b + 1 < nkb) issue(b + 1, buf ^ 1);
       if (b < wave_nkb) {
         const bf16 *Ks = smem + buf * S::STAGE;
         const bf16 *Vs = Ks + S::K_EL;
         f32x16 s[2];
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) s[t][r] = 0.f;
-          const bf16 *kp = Ks + (32 * t + perm32(ln)) * S::KP + 8 * kg;
-#pragma unroll
-          for (int c = 0; c < D / 16; ++c)
-            s[t] = mfma32(*reinterpret_cast<const bf16x8 *>(kp + 16 * c), qf[c], s[t]);
+        static_for<2>([&](auto t) {
+          static_for<16>([&](auto r) { s[t][int(r)] = 0.f; });
+          const bf16 *kp = Ks + 32 * t * D;
+          static_for<D / 16>([&](auto c) {
+            s[t] = mfma32(*reinterpret_cast<const bf16x8 *>(kp + koff[c]), qf[c], s[t]);
+          });
+        });
+        // keys past the row are masked only in blocks that reach past the
+        // wave's first row (the diagonal block of each row)
+        if (b * kFwdBN + kFwdBN - 1 > wave_qmin) {
+          static_for<2>([&](auto t) {
+            static_for<16>([&](auto r) {
+              const int kl = b * kFwdBN + 32 * t + 16 * (r >> 3) + 8 * kg + (r & 7);
+              if (kl > qloc) s[t][int(r)] = -INFINITY;
+            });
+          });
         }
-        const bool need_mask = b * kFwdBN + kFwdBN - 1 > wave_qmin;
         float mx = -INFINITY;
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            float x = s[t][r] * c2;
-            const int kl = b * kFwdBN + 32 * t + 16 * (r >> 3) + 8 * kg + (r & 7);
-            if (need_mask && kl > qloc) x = -INFINITY;
-            s[t][r] = x;
-            mx = fmaxf(mx, x);
-          }
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = fast_exp2(m_run - m_new);
-        m_run = m_new;
-        l_run *= alpha;
-#pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
+        static_for<2>([&](auto t) {
+          static_for<16>([&](auto r) { mx = fmaxf(mx, s[t][int(r)]); });
+        });
+        mx = fmaxf(mx, __shfl_xor(mx, 32)) * c2;       // row max of the scaled scores (log2 units)
+        // Lazy rescaling: the running max only moves when the block max exceeds
+        // it by more than 8 (a factor 256 in P).  The decision is per row, so
+        // rows stay independent of each other; the wave skips the multiply
+        // when no row moves.
+        const bool move = mx > m_run + 8.f;
+        if (__builtin_amdgcn_ballot_w64(move)) {
+          const float alpha = move ? fast_exp2(m_run - mx) : 1.f;
+          m_run = move ? mx : m_run;
+          l_run *= alpha;
+          static_for<D / 32>([&](auto dt) {
+            static_for<16>([&](auto r) { oacc[dt][int(r)] *= alpha; });
+          });
+        }
         bf16x8 pf[4];
         float ps = 0.f;
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const float p = fast_exp2(s[t][r] - m_new);
+        const float neg_m = -m_run;
+        static_for<2>([&](auto t) {
+          static_for<16>([&](auto r) {
+            const float p = fast_exp2(__builtin_fmaf(s[t][int(r)], c2, neg_m));
             ps += p;
             pf[2 * t + (r >> 3)][r & 7] = static_cast<bf16>(p);
-          }
+          });
+        });
         l_run += ps;
-#pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt) {
-          const bf16 *vp = Vs + (32 * dt + perm32(ln)) * S::VP + 8 * kg;
-#pragma unroll
-          for (int c = 0; c < 4; ++c)
-            oacc[dt] = mfma32(*reinterpret_cast<const bf16x8 *>(vp + 16 * c), pf[c], oacc[dt]);
-        }
+        static_for<D / 32>([&](auto dt) {
+          const bf16 *vp = Vs + 32 * dt * kFwdBN;
+          static_for<4>([&](auto c) {
+            oacc[dt] = mfma32(*reinterpret_cast<const bf16x8 *>(vp + voff_l[c]), pf[c], oacc[dt]);
+          });
+        });
       }
-      if (b + 1 < nkb) stash(buf ^ 1);
+      wait_vm();
       __syncthreads();
     }
 
@@ -342,12 +308,16 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
 // Host launcher.  `ws` is laid out as: header | items | Vt.
 static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
-FwdLayout fwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, int h_kv, int d) {
-  FwdLayout L;
-  // items <= rows*heads/64 (item covers >= 64 (row, head) pairs or ends a
+int64_t fwd_max_items(int64_t T, int64_t n, int64_t n_q, int h_q, int h_kv) {
+  // items <= rows*heads/64 (an item covers >= 64 (row, head) pairs or ends a
   // fragment) + fragments * head chunks.
   const int64_t frags = T + (int64_t)h_q * n;
-  L.max_items = n_q * (int64_t)h_q / 64 + frags * (int64_t)(h_kv + h_q / 4 + 1) + 1;
+  return n_q * (int64_t)h_q / 64 + frags * (int64_t)(h_kv + h_q / 4 + 1) + 1;
+}
+
+FwdLayout fwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, int h_kv, int d) {
+  FwdLayout L;
+  L.max_items = fwd_max_items(T, n, n_q, h_q, h_kv);
   L.pitch = vt_pitch(n_kv, n);
   L.hdr = 0;
   L.items = align256(kHdrSlots * sizeof(int32_t));
@@ -387,6 +357,26 @@ static int launch_fwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const int64
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(LIBRA_EHIP, "forward launch failed: %s", hipGetErrorString(e));
   return LIBRA_OK;
+}
+
+void enqueue_fwd_items(const int64_t *cu, int64_t n, const libra_tile_t *tiles, int64_t T,
+                       int h_q, int h_kv, int64_t n_q, int64_t n_kv, int32_t *hdr,
+                       FwdItem *items, int64_t max_items, hipStream_t st) {
+  hipLaunchKernelGGL(prep_fwd_kernel, dim3(1), dim3(kPrepThreads), 0, st, cu, n, tiles, T, h_q,
+                     h_kv, n_q, n_kv, hdr, items, max_items);
+}
+
+void enqueue_transpose(const void *src, const int64_t *cu, int64_t n, int64_t n_kv, int h_kv,
+                       int d, int64_t pitch, void *dst, hipStream_t st) {
+  const dim3 grid((unsigned)((n_kv + 63) / 64), h_kv);
+  if (d == 128)
+    hipLaunchKernelGGL(transpose_v_kernel<128>, grid, dim3(256), 0, st,
+                       static_cast<const bf16 *>(src), cu, n, n_kv, h_kv, pitch,
+                       static_cast<bf16 *>(dst));
+  else
+    hipLaunchKernelGGL(transpose_v_kernel<64>, grid, dim3(256), 0, st,
+                       static_cast<const bf16 *>(src), cu, n, n_kv, h_kv, pitch,
+                       static_cast<bf16 *>(dst));
 }
 
 int launch_fwd(const void *q, const void *k, const void *v, const int64_t *cu, int64_t n,
