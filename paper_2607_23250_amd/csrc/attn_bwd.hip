@@ -97,15 +97,18 @@ __global__ __launch_bounds__(kPrepThreads) void prep_bwd_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Pre-pass over the covered (row, head) pairs, 32 rows at a time:
-// D = rowsum(dO * O) and Q^T, dO^T as [h_q][D][nq_pad].
+// Pre-pass over the covered (row, head) pairs, 32 rows at a time: Q^T and
+// dO^T as [h_q][D][nq_pad], and per 32-row block of each head the 32 values
+// LSE * log2(e) followed by the 32 values D = rowsum(dO * O) ("stats",
+// [h_q][nq_pad / 32][64] floats, so one 256-byte load fetches both).
 constexpr int kTileSplit = 64;
 
 template <int D>
 __global__ __launch_bounds__(256) void bwd_pre_kernel(
     const bf16 *__restrict__ q, const bf16 *__restrict__ o, const bf16 *__restrict__ dout,
-    const libra_tile_t *__restrict__ tiles, int h_q, int64_t n_q, int64_t n_kv, int64_t nq_pad,
-    float *__restrict__ dvec, bf16 *__restrict__ qt, bf16 *__restrict__ dot) {
+    const float *__restrict__ lse, const libra_tile_t *__restrict__ tiles, int h_q, int64_t n_q,
+    int64_t n_kv, int64_t nq_pad, float *__restrict__ stats, bf16 *__restrict__ qt,
+    bf16 *__restrict__ dot) {
   __shared__ bf16 tq[kRows][D + 2];
   __shared__ bf16 tdo[kRows][D + 2];
   const int tid = threadIdx.x;
@@ -141,7 +144,11 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(
         acc += __shfl_xor(acc, 1);
         acc += __shfl_xor(acc, 2);
         acc += __shfl_xor(acc, 4);
-        if (part == 0 && row >= lo && row < hi) dvec[(size_t)h * n_q + row] = acc;
+        if (part == 0 && row >= lo && row < hi) {
+          float *st = stats + ((size_t)h * (nq_pad / kRows) + m) * 2 * kRows;
+          st[r] = lse[(size_t)h * n_q + row] * kLog2e;
+          st[kRows + r] = acc;
+        }
       }
       __syncthreads();
       for (int e = tid; e < D * kRows; e += 256) {
@@ -172,11 +179,27 @@ struct KvShape {
   static constexpr int TC = kRows / 8;      // 16-byte columns of a Q^T / dO^T row (4)
   static constexpr int Q_EL = kRows * D;
   static constexpr int T_EL = D * kRows;
-  static constexpr int STAGE_EL = 2 * Q_EL + 2 * T_EL;
+  static constexpr int F_EL = 2 * 2 * kRows;                 // 64 floats as bf16 slots
+  static constexpr int STAGE_EL = 2 * Q_EL + 2 * T_EL + F_EL;
+  static constexpr int NSTAGE = 4;                            // LDS ring of query blocks
   static constexpr int NQ = kRows * QC / 64 / kWaves;   // wave loads per Q (dO) tile
   static constexpr int NT = D * TC / 64 / kWaves;       // wave loads per Q^T (dO^T) tile
-  static constexpr size_t SMEM = 2 * STAGE_EL * sizeof(bf16) + 2 * 2 * kRows * sizeof(float);
+  static constexpr int LOADS = 2 * NQ + 2 * NT;         // per wave per step (+1 on wave 0)
+  static constexpr size_t SMEM = NSTAGE * STAGE_EL * sizeof(bf16);
 };
+
+// s_waitcnt vmcnt(N) for a compile-time N.
+template <int N>
+__device__ __forceinline__ void wait_vm_n() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+// Wait until at most k * L (k = 0, 1, 2) vector-memory operations are outstanding.
+template <int L>
+__device__ __forceinline__ void wait_stages(int k) {
+  if (k >= 2) wait_vm_n<2 * L>();
+  else if (k == 1) wait_vm_n<L>();
+  else wait_vm_n<0>();
+}
 
 // Walks the steps (32-row query block x query head) that attend one KV block:
 // tiles in list order, query blocks in row order, heads in order.
@@ -225,20 +248,36 @@ template <int D>
 __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
     const bf16 *__restrict__ k, const bf16 *__restrict__ v, const bf16 *__restrict__ q,
     const bf16 *__restrict__ dout, const bf16 *__restrict__ qt, const bf16 *__restrict__ dot,
-    const float *__restrict__ lse, const float *__restrict__ dvec,
-    const int64_t *__restrict__ cu, const libra_tile_t *__restrict__ tiles, int64_t T,
-    const BwdItem *__restrict__ items, int32_t *__restrict__ hdr, int h_q, int h_kv,
-    int64_t n_q, int64_t n_kv, int64_t nq_pad, float scale, float c2,
-    void *__restrict__ dk_out, void *__restrict__ dv_out, int accumulate) {
+    const float *__restrict__ stats, const int64_t *__restrict__ cu,
+    const libra_tile_t *__restrict__ tiles, int64_t T, const BwdItem *__restrict__ items,
+    int32_t *__restrict__ hdr, int h_q, int h_kv, int64_t n_q, int64_t n_kv, int64_t nq_pad,
+    float scale, float c2, void *__restrict__ dk_out, void *__restrict__ dv_out,
+    int accumulate) {
   using S = KvShape<D>;
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
-  float *fsm = reinterpret_cast<float *>(smem + 2 * S::STAGE_EL);   // [buf][lse2 | D][32]
   __shared__ int32_t s_item;
 
   const int tid = threadIdx.x, l = tid & 63, ln = l & 31, kg = l >> 5;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
   const int G = h_q / h_kv;
+  const int64_t nblk = nq_pad / kRows;
   int q_serve = blockIdx.x % kXcds, q_left = kXcds;
+  // per-lane LDS offsets (elements) of the operand reads
+  const int prow = perm32(ln);
+  int qoff[D / 16], toff[2];
+  static_for<D / 16>([&](auto c) { qoff[c] = prow * D + 8 * swz<S::QC>(prow, 2 * c + kg); });
+  static_for<2>([&](auto c) { toff[c] = prow * kRows + 8 * swz<S::TC>(prow, 2 * c + kg); });
+  // per-lane parts of the staging addresses (elements), fixed for the kernel
+  int q_lane[S::NQ];
+  int64_t t_lane[S::NT];
+  static_for<S::NQ>([&](auto u) {
+    const int r = (w + kWaves * u) * (64 / S::QC) + l / S::QC;
+    q_lane[u] = r * h_q * D + 8 * swz<S::QC>(r, l % S::QC);
+  });
+  static_for<S::NT>([&](auto u) {
+    const int r = (w + kWaves * u) * (64 / S::TC) + l / S::TC;
+    t_lane[u] = (int64_t)r * nq_pad + 8 * swz<S::TC>(r, l % S::TC);
+  });
 
   for (;;) {
     if (tid == 0) s_item = take_item(hdr, kBwdQ, q_serve, q_left);
@@ -253,101 +292,88 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
     const int kw0 = kloc0 + 32 * w;                   // first key of this wave
     const int kl = kw0 + ln;                          // this lane's key (sample-local)
     const bool key_ok = kl < len;
+    const bool wave_keys_ok = kw0 + 31 < len;
     const int64_t krow = key0 + kl;
 
     bf16x8 kf[D / 16], vf[D / 16];
-#pragma unroll
-    for (int c = 0; c < D / 16; ++c) {
+    static_for<D / 16>([&](auto c) {
       if (key_ok) {
         const size_t off = ((size_t)krow * h_kv + g) * D + 16 * c + 8 * kg;
         kf[c] = *reinterpret_cast<const bf16x8 *>(k + off);
         vf[c] = *reinterpret_cast<const bf16x8 *>(v + off);
       } else {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) { kf[c][i] = bf16(0.f); vf[c][i] = bf16(0.f); }
+        static_for<8>([&](auto i) { kf[c][int(i)] = bf16(0.f); vf[c][int(i)] = bf16(0.f); });
       }
-    }
+    });
     f32x16 dva[D / 32], dka[D / 32];
-#pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) { dva[dt][r] = 0.f; dka[dt][r] = 0.f; }
+    static_for<D / 32>([&](auto dt) {
+      static_for<16>([&](auto r) { dva[dt][int(r)] = 0.f; dka[dt][int(r)] = 0.f; });
+    });
 
-    // ---- staging of one step: Q, dO, Q^T, dO^T go global -> LDS directly
-    // (rows of the 32-row block outside the fragment are masked in the
-    // compute; Q^T / dO^T hold zeros there), LSE and D through registers.
-    float rl = 0.f, rd = 0.f;
-    auto issue = [&](const StepIter &st, int buf) {
+    // ---- one step = (32-row query block, head); its Q, dO, Q^T, dO^T and
+    // stats go global -> LDS into ring stage `sg` (rows of the block outside
+    // the fragment are masked in the compute; Q^T / dO^T hold zeros there)
+    auto issue = [&](const StepIter &st, int sg) {
       const int64_t m0 = st.m * kRows;
-      bf16 *Qs = smem + buf * S::STAGE_EL;
+      bf16 *Qs = smem + sg * S::STAGE_EL;
       bf16 *dOs = Qs + S::Q_EL;
       bf16 *Qts = dOs + S::Q_EL;
       bf16 *dOts = Qts + S::T_EL;
-      static_for<S::NQ>([&](auto u) {
-        const int wl = w + kWaves * u;
-        const int r = wl * (64 / S::QC) + l / S::QC;
-        const int col = swz<S::QC>(r, l % S::QC);
-        int64_t row = m0 + r;
-        row = row < n_q ? row : n_q - 1;
-        const size_t off = ((size_t)row * h_q + st.h) * D + 8 * col;
-        g2l16(q + off, Qs + wl * 512);
-        g2l16(dout + off, dOs + wl * 512);
-      });
+      bf16 *Fs = dOts + S::T_EL;
+      if (m0 + kRows <= n_q) {
+        const size_t qbase = ((size_t)m0 * h_q + st.h) * D;
+        static_for<S::NQ>([&](auto u) {
+          const int wl = w + kWaves * u;
+          g2l16(q + qbase + q_lane[u], Qs + wl * 512);
+          g2l16(dout + qbase + q_lane[u], dOs + wl * 512);
+        });
+      } else {
+        // the last block of the buffer: rows past it read the last row (masked)
+        static_for<S::NQ>([&](auto u) {
+          const int wl = w + kWaves * u;
+          const int r = wl * (64 / S::QC) + l / S::QC;
+          const int64_t row = m0 + r < n_q ? m0 + r : n_q - 1;
+          const size_t off = ((size_t)row * h_q + st.h) * D + 8 * swz<S::QC>(r, l % S::QC);
+          g2l16(q + off, Qs + wl * 512);
+          g2l16(dout + off, dOs + wl * 512);
+        });
+      }
+      const size_t tbase = (size_t)st.h * D * nq_pad + m0;
       static_for<S::NT>([&](auto u) {
         const int wl = w + kWaves * u;
-        const int r = wl * (64 / S::TC) + l / S::TC;
-        const int col = swz<S::TC>(r, l % S::TC);
-        const size_t off = ((size_t)st.h * D + r) * nq_pad + m0 + 8 * col;
-        g2l16(qt + off, Qts + wl * 512);
-        g2l16(dot + off, dOts + wl * 512);
+        g2l16(qt + tbase + t_lane[u], Qts + wl * 512);
+        g2l16(dot + tbase + t_lane[u], dOts + wl * 512);
       });
-      if (tid < kRows) {
-        const int lo_l = (int)(st.lo() - m0), hi_l = (int)(st.hi() - m0);
-        const bool ok = tid >= lo_l && tid < hi_l;
-        rl = ok ? lse[(size_t)st.h * n_q + m0 + tid] * kLog2e : 0.f;
-        rd = ok ? dvec[(size_t)st.h * n_q + m0 + tid] : 0.f;
-      }
+      if (w == 0 && l < 16) g2l16(stats + ((size_t)st.h * nblk + st.m) * 64 + 4 * l, Fs);
     };
-    auto stash_f = [&](int buf) {
-      if (tid < kRows) {
-        fsm[buf * 2 * kRows + tid] = rl;
-        fsm[buf * 2 * kRows + kRows + tid] = rd;
-      }
-    };
-    // per-lane LDS offsets (elements) of the operand reads
-    const int prow = perm32(ln);
-    int qoff[D / 16], toff[2];
-    static_for<D / 16>([&](auto c) { qoff[c] = prow * D + 8 * swz<S::QC>(prow, 2 * c + kg); });
-    static_for<2>([&](auto c) { toff[c] = prow * kRows + 8 * swz<S::TC>(prow, 2 * c + kg); });
 
-    StepIter cur{tiles, T, n_q, n_kv, key0, len, h_q, g, G, kloc0};
-    cur.start();
-    if (cur.valid) {
-      issue(cur, 0);
-      stash_f(0);
-    }
-    wait_vm();
-    __syncthreads();
-    int buf = 0;
+    StepIter iss{tiles, T, n_q, n_kv, key0, len, h_q, g, G, kloc0};
+    iss.start();
+    StepIter cur = iss;
+    int issued = 0, computed = 0;
     while (cur.valid) {
-      StepIter nxt = cur;
-      nxt.next();
-      if (nxt.valid) issue(nxt, buf ^ 1);
-      // ---- compute the current step from LDS buffer `buf`
+      // keep up to two steps in flight beyond the one computed now
+      while (iss.valid && issued < computed + S::NSTAGE - 1) {
+        issue(iss, issued % S::NSTAGE);
+        iss.next();
+        ++issued;
+      }
+      const int after = issued - 1 - computed;          // steps issued after this one
+      if (w == 0) wait_stages<S::LOADS + 1>(after); else wait_stages<S::LOADS>(after);
+      __syncthreads();
+
+      // ---- compute the step from ring stage computed % NSTAGE
       // rows of the block are m0 + iq, iq in [0, 32); row iq is valid for this
       // lane's key when lower <= iq < upper (inside the fragment and causal).
       const int64_t m0 = cur.m * kRows;
       const int lo_l = (int)(cur.lo() - m0), hi_l = (int)(cur.hi() - m0);
-      const int64_t qbase = cur.qla + (m0 - cur.fra);         // q_loc of row m0
-      const int64_t need = (int64_t)kl - qbase;               // first iq with q_loc >= kl
-      const int lower = (int)(need > lo_l ? (need < kRows ? need : kRows) : lo_l);
-      const int upper = key_ok ? hi_l : 0;
-      if ((int64_t)kw0 <= qbase + hi_l - 1) {
-        const bf16 *Qs = smem + buf * S::STAGE_EL;
+      const int64_t qb = cur.qla + (m0 - cur.fra);            // q_loc of row m0
+      if ((int64_t)kw0 <= qb + hi_l - 1) {
+        const bf16 *Qs = smem + (computed % S::NSTAGE) * S::STAGE_EL;
         const bf16 *dOs = Qs + S::Q_EL;
         const bf16 *Qts = dOs + S::Q_EL;
         const bf16 *dOts = Qts + S::T_EL;
-        const float *l2s = fsm + buf * 2 * kRows;
+        const float *l2s = reinterpret_cast<const float *>(dOts + S::T_EL);
         const float *dvs = l2s + kRows;
         f32x16 sa, pa;
         static_for<16>([&](auto r) { sa[int(r)] = 0.f; pa[int(r)] = 0.f; });
@@ -355,27 +381,34 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
           sa = mfma32(*reinterpret_cast<const bf16x8 *>(Qs + qoff[c]), kf[c], sa);
           pa = mfma32(*reinterpret_cast<const bf16x8 *>(dOs + qoff[c]), vf[c], pa);
         });
+        // keep the LDS reads a few MFMAs ahead (one wave per SIMD: nothing
+        // else hides their latency)
+        sched_pipeline<2 * (D / 16), 4>();
+        // interior blocks: every row inside the fragment and at or after every key
+        const bool full = lo_l == 0 && hi_l == kRows && wave_keys_ok && kw0 + 31 <= qb;
+        const int64_t need = (int64_t)kl - qb;                // first iq with q_loc >= kl
+        const int lower = full ? 0 : (int)(need > lo_l ? (need < kRows ? need : kRows) : lo_l);
+        const int upper = full ? kRows : (key_ok ? hi_l : 0);
         bf16x8 pb16[2], db16[2];
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
+        static_for<2>([&](auto hh) {
           const int iq0 = 16 * hh + 8 * kg;
           const f32x4 la = *reinterpret_cast<const f32x4 *>(l2s + iq0);
           const f32x4 lb = *reinterpret_cast<const f32x4 *>(l2s + iq0 + 4);
           const f32x4 da = *reinterpret_cast<const f32x4 *>(dvs + iq0);
           const f32x4 db = *reinterpret_cast<const f32x4 *>(dvs + iq0 + 4);
-#pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            const int r = 8 * hh + i;
-            const int iq = iq0 + i;
-            const bool ok = iq >= lower && iq < upper;
-            const float l2 = i < 4 ? la[i] : lb[i - 4];
-            const float dd = i < 4 ? da[i] : db[i - 4];
-            const float p = ok ? fast_exp2(sa[r] * c2 - l2) : 0.f;
-            const float ds = ok ? p * (pa[r] - dd) : 0.f;
-            pb16[hh][i] = static_cast<bf16>(p);
-            db16[hh][i] = static_cast<bf16>(ds);
-          }
-        }
+          static_for<8>([&](auto i) {
+            constexpr int r = 8 * hh + i;
+            const float l2 = i < 4 ? la[int(i) & 3] : lb[int(i) & 3];
+            const float dd = i < 4 ? da[int(i) & 3] : db[int(i) & 3];
+            float p = fast_exp2(__builtin_fmaf(sa[r], c2, -l2));
+            if (!full) {
+              const int iq = iq0 + i;
+              p = (iq >= lower && iq < upper) ? p : 0.f;
+            }
+            pb16[hh][int(i)] = static_cast<bf16>(p);
+            db16[hh][int(i)] = static_cast<bf16>(p * (pa[r] - dd));
+          });
+        });
         static_for<D / 32>([&](auto dt) {
           const bf16 *ap = dOts + 32 * dt * kRows;
           const bf16 *bp = Qts + 32 * dt * kRows;
@@ -384,47 +417,45 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
             dka[dt] = mfma32(*reinterpret_cast<const bf16x8 *>(bp + toff[c]), db16[c], dka[dt]);
           });
         });
+        sched_pipeline<4 * (D / 32), 4>();
       }
-      if (nxt.valid) stash_f(buf ^ 1);
-      wait_vm();
-      __syncthreads();
-      buf ^= 1;
-      cur = nxt;
+      ++computed;
+      cur.next();
     }
 
     // ---- write dK, dV for this wave's 32 keys
     if (key_ok) {
       const size_t base = ((size_t)krow * h_kv + g) * D + 8 * kg;
-#pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt)
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
+      static_for<D / 32>([&](auto dt) {
+        static_for<2>([&](auto hh) {
           const size_t off = base + 32 * dt + 16 * hh;
           if (accumulate) {
             float4 *dkp = reinterpret_cast<float4 *>(static_cast<float *>(dk_out) + off);
             float4 *dvp = reinterpret_cast<float4 *>(static_cast<float *>(dv_out) + off);
-#pragma unroll
-            for (int e = 0; e < 2; ++e) {
-              float4 a = dkp[e], b = dvp[e];
-              a.x += dka[dt][8 * hh + 4 * e + 0] * scale; b.x += dva[dt][8 * hh + 4 * e + 0];
-              a.y += dka[dt][8 * hh + 4 * e + 1] * scale; b.y += dva[dt][8 * hh + 4 * e + 1];
-              a.z += dka[dt][8 * hh + 4 * e + 2] * scale; b.z += dva[dt][8 * hh + 4 * e + 2];
-              a.w += dka[dt][8 * hh + 4 * e + 3] * scale; b.w += dva[dt][8 * hh + 4 * e + 3];
+            static_for<2>([&](auto e) {
+              constexpr int r0 = 8 * hh + 4 * e;
+              float4 a = dkp[e], bb = dvp[e];
+              a.x += dka[dt][r0 + 0] * scale; bb.x += dva[dt][r0 + 0];
+              a.y += dka[dt][r0 + 1] * scale; bb.y += dva[dt][r0 + 1];
+              a.z += dka[dt][r0 + 2] * scale; bb.z += dva[dt][r0 + 2];
+              a.w += dka[dt][r0 + 3] * scale; bb.w += dva[dt][r0 + 3];
               dkp[e] = a;
-              dvp[e] = b;
-            }
+              dvp[e] = bb;
+            });
           } else {
-            bf16x8 a, b;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-              a[i] = static_cast<bf16>(dka[dt][8 * hh + i] * scale);
-              b[i] = static_cast<bf16>(dva[dt][8 * hh + i]);
-            }
+            bf16x8 a, bb;
+            static_for<8>([&](auto i) {
+              a[int(i)] = static_cast<bf16>(dka[dt][8 * hh + i] * scale);
+              bb[int(i)] = static_cast<bf16>(dva[dt][8 * hh + i]);
+            });
             *reinterpret_cast<bf16x8 *>(static_cast<bf16 *>(dk_out) + off) = a;
-            *reinterpret_cast<bf16x8 *>(static_cast<bf16 *>(dv_out) + off) = b;
+            *reinterpret_cast<bf16x8 *>(static_cast<bf16 *>(dv_out) + off) = bb;
           }
-        }
+        });
+      });
     }
+    wait_vm_n<0>();
+    __syncthreads();   // the ring is reused by the next item
   }
 }
 
@@ -445,10 +476,10 @@ struct DqShape {
 template <int D>
 __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
     const bf16 *__restrict__ q, const bf16 *__restrict__ dout, const bf16 *__restrict__ k,
-    const bf16 *__restrict__ v, const bf16 *__restrict__ kt, const float *__restrict__ lse,
-    const float *__restrict__ dvec, const int64_t *__restrict__ cu,
-    const FwdItem *__restrict__ items, int32_t *__restrict__ hdr, int h_q, int h_kv,
-    int64_t n_q, int64_t n_kv, int64_t pitch, float c2, float scale, bf16 *__restrict__ dq) {
+    const bf16 *__restrict__ v, const bf16 *__restrict__ kt, const float *__restrict__ stats,
+    const int64_t *__restrict__ cu, const FwdItem *__restrict__ items,
+    int32_t *__restrict__ hdr, int h_q, int h_kv, int64_t n_q, int64_t n_kv, int64_t nq_pad,
+    int64_t pitch, float c2, float scale, bf16 *__restrict__ dq) {
   using S = DqShape<D>;
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
   __shared__ int32_t s_item;
@@ -488,8 +519,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
         qf[c] = *reinterpret_cast<const bf16x8 *>(q + off + 16 * c);
         of[c] = *reinterpret_cast<const bf16x8 *>(dout + off + 16 * c);
       }
-      l2 = lse[(size_t)head * n_q + row] * kLog2e;
-      dd_q = dvec[(size_t)head * n_q + row];
+      const float *st = stats + ((size_t)head * (nq_pad / kRows) + row / kRows) * 2 * kRows;
+      l2 = st[row % kRows];
+      dd_q = st[kRows + row % kRows];
     }
     f32x16 acc[D / 32];
 #pragma unroll
@@ -543,6 +575,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
                            dp[t]);
           });
         });
+        sched_pipeline<4 * (D / 16), 4>();
         // causal mask only in blocks that reach past the wave's first row
         if (b * kFwdBN + kFwdBN - 1 > wave_qmin) {
           static_for<2>([&](auto t) {
@@ -566,6 +599,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
                              dsf[c], acc[dt]);
           });
         });
+        sched_pipeline<4 * (D / 32), 4>();
       }
       wait_vm();
       __syncthreads();
@@ -600,8 +634,8 @@ BwdLayout bwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, i
   L.gmask = align256b(L.ext + (size_t)n * sizeof(int32_t));
   L.items = align256b(L.gmask + (size_t)n * sizeof(unsigned long long));
   L.qitems = align256b(L.items + (size_t)L.max_items * sizeof(BwdItem));
-  L.dvec = align256b(L.qitems + (size_t)L.max_qitems * sizeof(FwdItem));
-  L.qt = align256b(L.dvec + (size_t)h_q * n_q * sizeof(float));
+  L.stats = align256b(L.qitems + (size_t)L.max_qitems * sizeof(FwdItem));
+  L.qt = align256b(L.stats + (size_t)h_q * L.nq_pad * 2 * sizeof(float));
   L.dot = align256b(L.qt + (size_t)h_q * d * L.nq_pad * sizeof(bf16));
   L.kt = align256b(L.dot + (size_t)h_q * d * L.nq_pad * sizeof(bf16));
   L.total = align256b(L.kt + (size_t)h_kv * d * L.pitch * sizeof(bf16));
@@ -620,7 +654,7 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
   auto *gmask = reinterpret_cast<unsigned long long *>(ws + L.gmask);
   BwdItem *items = reinterpret_cast<BwdItem *>(ws + L.items);
   FwdItem *qitems = reinterpret_cast<FwdItem *>(ws + L.qitems);
-  float *dvec = reinterpret_cast<float *>(ws + L.dvec);
+  float *stats = reinterpret_cast<float *>(ws + L.stats);
   bf16 *qt = reinterpret_cast<bf16 *>(ws + L.qt);
   bf16 *dot = reinterpret_cast<bf16 *>(ws + L.dot);
   bf16 *kt = reinterpret_cast<bf16 *>(ws + L.kt);
@@ -646,30 +680,33 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
                        h_kv, n_q, n_kv, hdr, ext, gmask, items, L.max_items);
     enqueue_fwd_items(cu, n, tiles, T, h_q, h_kv, n_q, n_kv, hdr, qitems, L.max_qitems, st);
     {
-      // Q^T / dO^T are zero outside the covered rows: query blocks of the
-      // dK/dV kernel contract over all 32 rows of a block
+      // Q^T / dO^T (and the stats) are zero outside the covered rows: query
+      // blocks of the dK/dV kernel contract over all 32 rows of a block
       const int64_t n16 = (int64_t)h_q * D * L.nq_pad * (int64_t)sizeof(bf16) / 16;
       const unsigned blocks = (unsigned)std::min<int64_t>((n16 + 255) / 256, 4096);
       hipLaunchKernelGGL(zero_kernel, dim3(blocks), dim3(256), 0, st, reinterpret_cast<uint4 *>(qt),
                          n16);
       hipLaunchKernelGGL(zero_kernel, dim3(blocks), dim3(256), 0, st,
                          reinterpret_cast<uint4 *>(dot), n16);
+      const int64_t s16 = (int64_t)h_q * L.nq_pad * 2 * (int64_t)sizeof(float) / 16;
+      hipLaunchKernelGGL(zero_kernel, dim3((unsigned)std::min<int64_t>((s16 + 255) / 256, 4096)),
+                         dim3(256), 0, st, reinterpret_cast<uint4 *>(stats), s16);
     }
     hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)(T * kTileSplit)), dim3(256), 0, st, q, o,
-                       dout, tiles, h_q, n_q, n_kv, L.nq_pad, dvec, qt, dot);
+                       dout, lse, tiles, h_q, n_q, n_kv, L.nq_pad, stats, qt, dot);
     enqueue_transpose(k, cu, n, n_kv, h_kv, D, L.pitch, kt, st);
     int dev = 0, cus = 256;
     hipGetDevice(&dev);
     hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (tm_kv) hipEventRecord(tm_kv->begin, st);
     hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(cus), dim3(kThreads), KvShape<D>::SMEM, st, k,
-                       v, q, dout, qt, dot, lse, dvec, cu, tiles, T, items, hdr, h_q, h_kv, n_q,
-                       n_kv, L.nq_pad, scale, scale * kLog2e, dk, dv, accumulate ? 1 : 0);
+                       v, q, dout, qt, dot, stats, cu, tiles, T, items, hdr, h_q, h_kv, n_q, n_kv,
+                       L.nq_pad, scale, scale * kLog2e, dk, dv, accumulate ? 1 : 0);
     if (tm_kv) hipEventRecord(tm_kv->end, st);
     if (tm_q) hipEventRecord(tm_q->begin, st);
     hipLaunchKernelGGL(attn_bwd_dq_kernel<D>, dim3(cus), dim3(kThreads), DqShape<D>::SMEM, st, q,
-                       dout, k, v, kt, lse, dvec, cu, qitems, hdr, h_q, h_kv, n_q, n_kv, L.pitch,
-                       scale * kLog2e, scale, dq);
+                       dout, k, v, kt, stats, cu, qitems, hdr, h_q, h_kv, n_q, n_kv, L.nq_pad,
+                       L.pitch, scale * kLog2e, scale, dq);
     if (tm_q) hipEventRecord(tm_q->end, st);
   }
   const hipError_t e = hipGetLastError();

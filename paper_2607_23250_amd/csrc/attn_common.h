@@ -174,6 +174,20 @@ __device__ __forceinline__ void g2l16(const void *g, bf16 *lds) {
 // Wait for this wave's outstanding global loads (including global -> LDS).
 __device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// Scheduling hint for a run of N MFMAs that each consume one 16-byte LDS
+// read: issue AHEAD reads first, then alternate one MFMA with one read, so
+// that every read is in flight while earlier MFMAs execute.
+template <int N, int AHEAD>
+__device__ __forceinline__ void sched_pipeline() {
+  __builtin_amdgcn_sched_group_barrier(0x100, AHEAD, 0);   // DS reads
+#pragma unroll
+  for (int i = 0; i < N - AHEAD; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);      // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);      // DS read
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, AHEAD, 0);
+}
+
 // Compile-time loop: f(std::integral_constant<int, i>{}) for i in [0, N).  Register
 // arrays indexed this way are kept in registers (a runtime-indexed or
 // captured array can end up in scratch memory).
@@ -214,7 +228,7 @@ struct FwdLayout {
   int64_t max_items = 0, pitch = 0;
 };
 struct BwdLayout {
-  size_t hdr = 0, ext = 0, gmask = 0, items = 0, qitems = 0, dvec = 0, qt = 0, dot = 0, kt = 0,
+  size_t hdr = 0, ext = 0, gmask = 0, items = 0, qitems = 0, stats = 0, qt = 0, dot = 0, kt = 0,
          total = 0;
   int64_t max_items = 0, max_qitems = 0, nq_pad = 0, pitch = 0;
 };
