@@ -10,8 +10,8 @@ asynchronous planner does.
 Default workload: one GPU's CP=16 head+tail share of a 1,048,576-token pack
 (Qwen3-30B-A3B attention: 32 query heads, 4 KV heads, head_dim 128; 65,536
 query rows against up to 1M causal keys, one ~900K-token sample), planned
-over 16 virtual workers.  ``--config k`` selects another of the five seeded
-workloads.  Inputs are seeded synthetic tensors resident in HBM before the
+over 16 virtual workers.  ``--workload NAME`` selects another of the five
+seeded workloads.  Inputs are seeded synthetic tensors resident in HBM before the
 timed region starts.
 
 Prints ONE JSON line: useful causal-masked attention TFLOP/s of fwd+bwd
@@ -45,10 +45,31 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", type=int, default=5, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--workload", default="1M-cp16-share-qwen3-30b-a3b",
+                    help="one of the seeded workloads: 4K-h2-kv1-d64, 32K-qwen3-8b, "
+                         "pool8x64K-qwen3-30b-a3b, 256K-cp16-share-qwen3-235b-a22b, "
+                         "1M-cp16-share-qwen3-30b-a3b")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="time budget of the CPU oracle baseline (0 disables it)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain elementwise copy of a known size (1 GiB read, "
+                         "1 GiB written, 3 launches): the reference the HBM byte counters "
+                         "of the profiler are scaled by")
     return ap.parse_args()
+
+
+def copy_calibration():
+    import torch
+    n = 1 << 28                                      # 2^28 fp32 = 1 GiB
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration": {"kernel": "elementwise neg (copy)", "launches": 3,
+                                           "read_bytes": 4 * n, "write_bytes": 4 * n}}),
+          flush=True)
 
 
 def plan(pl, w, q_ranges=None):
@@ -67,10 +88,11 @@ def launch_sets(w, full_tiles, share_tiles):
     return [full_tiles]
 
 
-def traffic_entry(kernel: str, launches_per_step: int):
-    """HBM bytes per launch from committed rocprofv3 PMC summaries, or None when
-    missing or taken on a different kernel source."""
-    path = os.path.join(ROOT, "profiles", f"{kernel}_traffic.json")
+def traffic_entry(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 PMC summary of this
+    kernel on this workload, or None when missing or taken on a different
+    kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}__{workload}__traffic.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
@@ -115,13 +137,16 @@ def main():
         print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
               "(the multi-GPU exchange of the paper is out of scope here)", file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
     import torch
     import paper_2607_23250_amd as pl
     import workloads as wl
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
-    w = wl.config(args.config)
+    w = wl.workload(args.workload)
     full_tiles, loads = plan(pl, w)
     share_tiles = plan(pl, w, w.q_ranges)[0] if w.q_ranges is not None else None
     sets = launch_sets(w, full_tiles, share_tiles)
@@ -223,7 +248,7 @@ def main():
     achieved = kv_launch_flops / (kv_launch_ms * 1e-3) / 1e12
     dq_launch_ms = dq_ms / max(n_dq, 1)
     fwd_achieved = (fwd_flops / len(sets)) / (fwd_main_ms / max(n_fwd, 1) * 1e-3) / 1e12
-    traffic = traffic_entry("attn_bwd_dkdv_kernel", len(sets))
+    traffic = traffic_entry("attn_bwd_dkdv_kernel", w.name)
 
     out = {
         "metric": METRIC,

@@ -75,8 +75,8 @@ def test_bwd_small_random(seed):
 
 
 def test_fwd_config1_full():
-    w = wl.config(1)
-    say(f"[fwd cfg1] {w.name} samples={len(w.lengths)}")
+    w = wl.workload(wl.W_4K)
+    say(f"[fwd 4K] {w.name} samples={len(w.lengths)}")
     tiles, _ = plan(w)
     q, k, v, _ = _inputs(w)
     o, lse = fwd(w, tiles, *_dev(q, k, v), cu_dev(w))
@@ -87,8 +87,8 @@ def test_fwd_config1_full():
 
 
 def test_fwd_bwd_config2_quarter_full():
-    w = wl.config(2, scale=4)
-    say(f"[fwd+bwd cfg2/4] {w.name} samples={len(w.lengths)}")
+    w = wl.workload(wl.W_32K, scale=4)
+    say(f"[fwd+bwd 32K/4] {w.name} samples={len(w.lengths)}")
     tiles, _ = plan(w)
     q, k, v, do = _inputs(w)
     qd, kd, vd, dod = _dev(q, k, v, do)
@@ -112,7 +112,7 @@ def test_fwd_independent_of_plan_and_worker_split():
     """Rows and heads are computed independently of how tiles group them:
     every plan, and every split of a plan into per-worker launches, gives
     bit-identical O and LSE."""
-    w = wl.config(2, scale=4)
+    w = wl.workload(wl.W_32K, scale=4)
     say(f"[plan invariance] {w.name}/4")
     q, k, v, _ = _inputs(w)
     qd, kd, vd = _dev(q, k, v)
@@ -137,7 +137,7 @@ def test_fwd_independent_of_plan_and_worker_split():
 
 
 def test_fwd_packed_equals_unpacked():
-    w = wl.config(2, scale=4)
+    w = wl.workload(wl.W_32K, scale=4)
     say(f"[packed == unpacked] {w.name}/4")
     tiles, _ = plan(w)
     q, k, v, _ = _inputs(w)
@@ -158,7 +158,7 @@ def test_fwd_packed_equals_unpacked():
 
 
 def test_fwd_deterministic():
-    w = wl.config(2, scale=2)
+    w = wl.workload(wl.W_32K, scale=2)
     say(f"[determinism] {w.name}/2")
     tiles, _ = plan(w)
     q, k, v, _ = _dev(*_inputs(w))

@@ -1,14 +1,14 @@
 """GPU parity on the five workloads, in the launch configuration bench.py times.
 
-* reduced replicas of configs 3-5 (same generator, every token count and the
+* reduced replicas of the pool, 256K-share and 1M-share workloads (same generator, every token count and the
   block size divided by a power of two): every output element against the
   float64 oracle (gradients: the 2e-2 bound, or twice the error of plain bf16
   PyTorch when that is larger -- the paper's criterion, Sec. 6.6);
-* full-size configs 2-5: O, LSE and dQ of sampled query rows (all heads),
+* the four large workloads at full size: O, LSE and dQ of sampled query rows (all heads),
   which the oracle computes row by row, and dK / dV from a second backward
   whose dO is zero except on those rows (then only those rows contribute, and
   the oracle computes the result exactly);
-* full-size configs 2-5 with K = 0: every row's O is the prefix mean of V,
+* the same four with K = 0: every row's O is the prefix mean of V,
   LSE = ln(q_loc + 1), dQ = 0 and dV has a closed form (a reverse prefix sum
   of dO / (q_loc + 1)), so every output element is checked at full size.
 """
@@ -28,9 +28,9 @@ pytestmark = pytest.mark.gpu
 
 
 @functools.lru_cache(maxsize=4)
-def _tensors(k, scale=1):
+def _tensors(name, scale=1):
     """Seeded inputs of a workload (cached: the largest take tens of seconds to draw)."""
-    w = wl.config(k, scale=scale)
+    w = wl.workload(name, scale=scale)
     return wl.tensors(w.seed, w.n_q_rows, w.n_kv_rows, w.h_q, w.h_kv, w.d)
 
 
@@ -64,11 +64,11 @@ def _run(w, sets, q, k, v, do, accumulate=None):
     return o, lse, dq, dk, dv
 
 
-@pytest.mark.parametrize("k,scale", [(3, 16), (4, 16), (5, 64)])
-def test_replica_full_parity(k, scale):
-    w = wl.config(k, scale=scale)
+@pytest.mark.parametrize("name,scale", [(wl.W_POOL, 16), (wl.W_256K, 16), (wl.W_1M, 64)])
+def test_replica_full_parity(name, scale):
+    w = wl.workload(name, scale=scale)
     sets = _launch_sets(w)
-    say(f"[replica cfg{k}/{scale}] rows={w.n_q_rows} keys={w.n_kv_rows} samples={len(w.lengths)} "
+    say(f"[replica {name}/{scale}] rows={w.n_q_rows} keys={w.n_kv_rows} samples={len(w.lengths)} "
         f"max={max(w.lengths)} launches={len(sets)}")
     q, kk, v, do = wl.tensors(w.seed, w.n_q_rows, w.n_kv_rows, w.h_q, w.h_kv, w.d)
     o, lse, dq, dk, dv = _run(w, sets, q, kk, v, do, accumulate=True)
@@ -107,14 +107,14 @@ def _sample_rows(w, sets, n_random, seed):
     return np.array(sorted(r for r in rows if 0 <= r < len(pos)), dtype=np.int64)
 
 
-@pytest.mark.parametrize("k", [2, 3, 4, 5])
-def test_full_size_sampled_rows(k):
-    w = wl.config(k)
+@pytest.mark.parametrize("name", wl.WORKLOADS[1:])
+def test_full_size_sampled_rows(name):
+    w = wl.workload(name)
     sets = _launch_sets(w)
-    rows = _sample_rows(w, sets, 8 if k == 5 else 16, seed=k)
-    say(f"[full cfg{k}] rows={w.n_q_rows} keys={w.n_kv_rows} launches={len(sets)} "
+    rows = _sample_rows(w, sets, 8 if name == wl.W_1M else 16, seed=w.seed)
+    say(f"[full {name}] rows={w.n_q_rows} keys={w.n_kv_rows} launches={len(sets)} "
         f"sampled rows={len(rows)}")
-    q, kk, v, do = _tensors(k)
+    q, kk, v, do = _tensors(name)
     o, lse, dq, _, _ = _run(w, sets, q, kk, v, do)
     pos = w.q_positions()
     O, LSE = oa.attention_fwd(q, kk, v, w.lengths, pos, rows=rows)
@@ -135,12 +135,12 @@ def test_full_size_sampled_rows(k):
     check("dV probe", to_np(dv2[:, g]), dV[:, g])
 
 
-@pytest.mark.parametrize("k", [2, 3, 4, 5])
-def test_full_size_zero_k_closed_forms(k):
-    w = wl.config(k)
+@pytest.mark.parametrize("name", wl.WORKLOADS[1:])
+def test_full_size_zero_k_closed_forms(name):
+    w = wl.workload(name)
     sets = _launch_sets(w)
-    say(f"[full cfg{k} K=0] rows={w.n_q_rows} keys={w.n_kv_rows} launches={len(sets)}")
-    q, kk, v, do = _tensors(k)
+    say(f"[full {name} K=0] rows={w.n_q_rows} keys={w.n_kv_rows} launches={len(sets)}")
+    q, kk, v, do = _tensors(name)
     kk = torch.zeros_like(kk)
     o, lse, dq, dk, dv = _run(w, sets, q, kk, v, do, accumulate=True)
     pos = w.q_positions()

@@ -172,7 +172,7 @@ def test_gradient_column_sums(seed):
 def test_row_subsets_and_sparse_dout():
     """Rows computed alone equal the same rows of a full run; a dO that is zero
     off the chosen rows gives the same dK/dV as restricting to those rows."""
-    w = wl.config(4, scale=64)          # 4096-token pack, CP=16 share of rank 0
+    w = wl.workload(wl.W_256K, scale=64)          # 4096-token pack, CP=16 share of rank 0
     q_all, k, v, do_all = wl.tensors(4, w.n_kv_rows, w.n_kv_rows, w.h_q, w.h_kv, w.d)
     pos_share = w.q_positions()
     q, do = q_all[pos_share], do_all[pos_share]
@@ -194,9 +194,9 @@ def test_row_subsets_and_sparse_dout():
     np.testing.assert_allclose(dV1, dV2, atol=1e-12)
 
 
-@pytest.mark.parametrize("k", [1, 2, 4])
-def test_useful_pairs_equal_plan_cost(k):
-    w = wl.config(k)
+@pytest.mark.parametrize("name", [wl.W_4K, wl.W_32K, wl.W_256K])
+def test_useful_pairs_equal_plan_cost(name):
+    w = wl.workload(name)
     cfg = op.PlanCfg(B=w.B, H=w.H, P=w.P, CP=w.CP, h_q=w.h_q, h_kv=w.h_kv, d=w.d)
     tiles = op.build_tiles(cfg, w.lengths, w.pack_tokens, w.q_ranges)
     assert sum(t.cost for t in tiles) == w.h_q * oa.useful_pairs(w.lengths, w.q_positions())
@@ -207,7 +207,7 @@ def test_bf16_reference_tracks_the_oracle():
     allowance) computes the same attention, to bf16 accuracy, on a subset of
     rows too."""
     from oracle.bf16_reference import attention_bf16
-    w = wl.config(4, scale=64)
+    w = wl.workload(wl.W_256K, scale=64)
     q, k, v, do = wl.tensors(4, w.n_q_rows, w.n_kv_rows, w.h_q, w.h_kv, w.d)
     pos = w.q_positions()
     O, dQ, dK, dV = attention_bf16(q, k, v, do, w.lengths, pos)

@@ -46,9 +46,9 @@ def test_costs_match_brute_force(seed):
         assert 0 < t.q_end - t.q_begin <= w.B
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
-def test_total_cost_closed_form(k):
-    w = wl.config(k)
+@pytest.mark.parametrize("name", wl.WORKLOADS)
+def test_total_cost_closed_form(name):
+    w = wl.workload(name)
     tiles = op.build_tiles(_cfg(w), w.lengths, w.pack_tokens)
     total = sum(t.cost for t in tiles)
     assert total == w.h_q * sum(n * (n + 1) // 2 for n in w.lengths)
@@ -148,7 +148,7 @@ def test_against_exhaustive_optimum(seed):
 
 
 def test_q_ranges_select_whole_blocks():
-    w = wl.config(4, scale=16)       # 16384-token pack, CP=16 share of rank 0
+    w = wl.workload(wl.W_256K, scale=16)       # 16384-token pack, CP=16 share of rank 0
     cfg = _cfg(w)
     full = op.build_tiles(cfg, w.lengths, w.pack_tokens)
     share = op.build_tiles(cfg, w.lengths, w.pack_tokens, w.q_ranges)

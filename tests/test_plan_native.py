@@ -36,17 +36,17 @@ def _same(native, oracle):
     assert [int(x) for x in loads] == list(oloads)
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
-def test_configs_bit_exact(k):
-    w = wl.config(k)
+@pytest.mark.parametrize("name", wl.WORKLOADS)
+def test_workloads_bit_exact(name):
+    w = wl.workload(name)
     _same(_native(w), _oracle(w))
     if w.q_ranges is not None:
         _same(_native(w, w.q_ranges), _oracle(w, w.q_ranges))
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
-def test_configs_meet_load_target(k):
-    w = wl.config(k)
+@pytest.mark.parametrize("name", wl.WORKLOADS)
+def test_workloads_meet_load_target(name):
+    w = wl.workload(name)
     tiles, loads = _native(w)
     assert w.V * loads.max() / loads.sum() <= 1.05
 
@@ -82,7 +82,7 @@ def test_random_q_ranges_bit_exact(seed):
 
 
 def test_size_query_and_enospc():
-    w = wl.config(2)
+    w = wl.workload(wl.W_32K)
     tiles, _ = _native(w)
     import ctypes
     L = pl.lib()

@@ -36,8 +36,8 @@ from typing import List, Optional, Sequence, Tuple
 import numpy as np
 
 __all__ = [
-    "LengthLaw", "Workload", "draw_length", "pack_lengths", "config",
-    "CONFIG_IDS", "tensors", "tiny_random",
+    "LengthLaw", "Workload", "draw_length", "pack_lengths", "workload", "WORKLOADS",
+    "W_4K", "W_32K", "W_POOL", "W_256K", "W_1M", "tensors", "tiny_random",
 ]
 
 
@@ -143,7 +143,14 @@ class Workload:
         return np.concatenate([np.arange(b, e, dtype=np.int64) for b, e in self.q_ranges])
 
 
-CONFIG_IDS = (1, 2, 3, 4, 5)
+# The five seeded workloads, by name (token counts, model whose attention
+# shapes they take).
+W_4K = "4K-h2-kv1-d64"
+W_32K = "32K-qwen3-8b"
+W_POOL = "pool8x64K-qwen3-30b-a3b"
+W_256K = "256K-cp16-share-qwen3-235b-a22b"
+W_1M = "1M-cp16-share-qwen3-30b-a3b"
+WORKLOADS = (W_4K, W_32K, W_POOL, W_256K, W_1M)
 
 
 def _share_ranges(L: int, cp: int, rank: int = 0) -> List[Tuple[int, int]]:
@@ -153,36 +160,40 @@ def _share_ranges(L: int, cp: int, rank: int = 0) -> List[Tuple[int, int]]:
     return [(a * c, (a + 1) * c), (b * c, (b + 1) * c)]
 
 
-def config(k: int, scale: int = 1, rank: int = 0) -> Workload:
-    """The five seeded workloads (config ``k`` uses length seed ``k``).
+def workload(name: str, scale: int = 1, rank: int = 0) -> Workload:
+    """One of the five seeded workloads of ``WORKLOADS`` (the i-th uses length
+    seed i + 1).
 
     ``scale`` > 1 divides every token count (pack size, forced sample, Pareto
     floor, cap, block size ``B``) by ``scale`` while keeping heads and ``H``;
     it builds the reduced replicas the parity tests check in full.  ``rank`` picks the CP
-    rank whose head+tail share is measured in configs 4 and 5.
+    rank whose head+tail share is measured in the two CP-share workloads.
     """
+    if name not in WORKLOADS:
+        raise ValueError(f"unknown workload {name!r}; one of {WORKLOADS}")
+    k = WORKLOADS.index(name) + 1
     rng = np.random.default_rng(k)
     s = int(scale)
     if k == 1:
         law = LengthLaw(median=644, sigma=1.0)
         packs = [pack_lengths(rng, law, 4096 // s)]
-        return Workload("cfg1-4K-h2-kv1-d64", k, packs, 2, 1, 64, B=256 // s, H=2, CP=4,
+        return Workload(W_4K, k, packs, 2, 1, 64, B=256 // s, H=2, CP=4,
                         backward=False)
     if k == 2:
         law = LengthLaw(median=644, sigma=1.5)
         packs = [pack_lengths(rng, law, 32768 // s, forced=[16384 // s])]
-        return Workload("cfg2-32K-qwen3-8b", k, packs, 32, 8, 128, B=2048 // s, H=2, CP=8)
+        return Workload(W_32K, k, packs, 32, 8, 128, B=2048 // s, H=2, CP=8)
     if k == 3:
         law = LengthLaw(median=644, sigma=1.5, w_lognormal=0.95, pareto_alpha=1.1,
                         pareto_xmin=8192 / s, cap=65536 // s)
         packs = [pack_lengths(rng, law, 65536 // s) for _ in range(8)]
-        return Workload("cfg3-pool8x64K-qwen3-30b-a3b", k, packs, 32, 4, 128, B=4096 // s,
+        return Workload(W_POOL, k, packs, 32, 4, 128, B=4096 // s,
                         H=2, CP=1, per_worker=True)
     if k == 4:
         L = 262144 // s
         law = LengthLaw(median=644, sigma=1.5)
         packs = [pack_lengths(rng, law, L, forced=[200000 // s])]
-        return Workload("cfg4-256K-cp16-share-qwen3-235b-a22b", k, packs, 64, 4, 128,
+        return Workload(W_256K, k, packs, 64, 4, 128,
                         B=4096 // s, H=2, CP=16, q_ranges=_share_ranges(L, 16, rank),
                         notes=["lognormal sigma=1.5 assumed", "V=16 assumed"])
     if k == 5:
@@ -190,10 +201,10 @@ def config(k: int, scale: int = 1, rank: int = 0) -> Workload:
         law = LengthLaw(median=644, sigma=2.0, w_lognormal=0.95, pareto_alpha=1.05,
                         pareto_xmin=32768 / s)
         packs = [pack_lengths(rng, law, L, forced=[900000 // s])]
-        return Workload("cfg5-1M-cp16-share-qwen3-30b-a3b", k, packs, 32, 4, 128,
+        return Workload(W_1M, k, packs, 32, 4, 128,
                         B=8192 // s, H=2, CP=16, q_ranges=_share_ranges(L, 16, rank),
                         notes=["mixture weights 0.95/0.05 assumed"])
-    raise ValueError(f"unknown config {k}")
+    raise AssertionError(name)
 
 
 def tensors(seed: int, n_q: int, n_k: int, h_q: int, h_kv: int, d: int,
