@@ -12,17 +12,17 @@
 //     over the 32-row query blocks of the tiles that attend them and over the
 //     query heads of the KV group.  S and dP are computed with queries on M
 //     (lane = key), exactly the operand layout that dV^T = dO^T P and
-//     dK^T = Q^T dS need.  Query blocks are staged in LDS double-buffered,
-//     the next one loaded while the current one is computed.
+//     dK^T = Q^T dS need; the dO^T / Q^T operands come from the same
+//     row-major LDS tiles through the LDS transpose reads.  Query blocks are
+//     staged in an LDS ring, up to seven ahead of the one computed.
 //   * dQ, query-stationary, shaped like the forward: S^T = K Q^T and
 //     dP^T = V dO^T (lane = query), dS^T = P^T * (dP^T - D), then
 //     dQ^T += K^T dS^T.  It recomputes S and dP instead of accumulating dQ
 //     across key blocks with atomics: on long samples that accumulation is
 //     read-modify-write traffic of 4 bytes x d per (32 queries x 128 keys)
 //     per head, which would bound the whole backward by HBM.
-// Preparation: D = rowsum(dO * O), transposed Q^T / dO^T of the covered rows
-// and a padded transposed K^T (every MFMA operand is read from LDS as 16
-// contiguous bytes), plus the two work-item lists, longest first.
+// Preparation: D = rowsum(dO * O), a padded transposed K^T for the dQ
+// kernel, plus the two work-item lists, longest first.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -97,70 +97,46 @@ __global__ __launch_bounds__(kPrepThreads) void prep_bwd_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Pre-pass over the covered (row, head) pairs, 32 rows at a time: Q^T and
-// dO^T as [h_q][D][nq_pad], and per 32-row block of each head the 32 values
-// LSE * log2(e) followed by the 32 values D = rowsum(dO * O) ("stats",
-// [h_q][nq_pad / 32][64] floats, so one 256-byte load fetches both).
+// Pre-pass over the covered (row, head) pairs, 32 rows at a time: per 32-row
+// block of each head the 32 values LSE * log2(e) followed by the 32 values
+// D = rowsum(dO * O) ("stats", [h_q][nq_pad / 32][64] floats, so one
+// 256-byte load fetches both).
 constexpr int kTileSplit = 64;
 
 template <int D>
 __global__ __launch_bounds__(256) void bwd_pre_kernel(
-    const bf16 *__restrict__ q, const bf16 *__restrict__ o, const bf16 *__restrict__ dout,
-    const float *__restrict__ lse, const libra_tile_t *__restrict__ tiles, int h_q, int64_t n_q,
-    int64_t n_kv, int64_t nq_pad, float *__restrict__ stats, bf16 *__restrict__ qt,
-    bf16 *__restrict__ dot) {
-  __shared__ bf16 tq[kRows][D + 2];
-  __shared__ bf16 tdo[kRows][D + 2];
+    const bf16 *__restrict__ o, const bf16 *__restrict__ dout, const float *__restrict__ lse,
+    const libra_tile_t *__restrict__ tiles, int h_q, int64_t n_q, int64_t n_kv,
+    int64_t nq_pad, float *__restrict__ stats) {
   const int tid = threadIdx.x;
   const libra_tile_t tl = tiles[blockIdx.x / kTileSplit];
   if (!tile_ok(tl, n_q, n_kv, h_q)) return;
   const int64_t ra = tl.q_row, rb = tl.q_row + (tl.q_end - tl.q_begin);
+  // 8 threads per row, 32 rows per pass
+  const int r = tid >> 3, part = tid & 7;
   for (int64_t m = ra / kRows + blockIdx.x % kTileSplit; m * kRows < rb; m += kTileSplit) {
-    const int64_t lo = m * kRows > ra ? m * kRows : ra;
-    const int64_t hi = (m + 1) * kRows < rb ? (m + 1) * kRows : rb;
+    const int64_t row = m * kRows + r;
+    const bool ok = row >= ra && row < rb;
     for (int h = tl.head_begin; h < tl.head_end; ++h) {
-      for (int ci = tid; ci < kRows * D / 2; ci += 256) {
-        const int r = ci / (D / 2), c2 = ci % (D / 2);
-        const int64_t row = m * kRows + r;
-        uint32_t qv = 0, dv = 0;
-        if (row >= lo && row < hi) {
-          const size_t off = ((size_t)row * h_q + h) * D + 2 * c2;
-          qv = *reinterpret_cast<const uint32_t *>(q + off);
-          dv = *reinterpret_cast<const uint32_t *>(dout + off);
-        }
-        *reinterpret_cast<uint32_t *>(&tq[r][2 * c2]) = qv;
-        *reinterpret_cast<uint32_t *>(&tdo[r][2 * c2]) = dv;
+      float acc = 0.f;
+      if (ok) {
+        const size_t off = ((size_t)row * h_q + h) * D + part * (D / 8);
+        static_for<D / 64>([&](auto c) {
+          const bf16x8 ov = *reinterpret_cast<const bf16x8 *>(o + off + 8 * c);
+          const bf16x8 dv = *reinterpret_cast<const bf16x8 *>(dout + off + 8 * c);
+          static_for<8>([&](auto i) {
+            acc += static_cast<float>(ov[int(i)]) * static_cast<float>(dv[int(i)]);
+          });
+        });
       }
-      {
-        const int r = tid >> 3, part = tid & 7;
-        const int64_t row = m * kRows + r;
-        float acc = 0.f;
-        if (row >= lo && row < hi) {
-          const size_t off = ((size_t)row * h_q + h) * D + part * (D / 8);
-#pragma unroll
-          for (int i = 0; i < D / 8; ++i)
-            acc += static_cast<float>(o[off + i]) * static_cast<float>(dout[off + i]);
-        }
-        acc += __shfl_xor(acc, 1);
-        acc += __shfl_xor(acc, 2);
-        acc += __shfl_xor(acc, 4);
-        if (part == 0 && row >= lo && row < hi) {
-          float *st = stats + ((size_t)h * (nq_pad / kRows) + m) * 2 * kRows;
-          st[r] = lse[(size_t)h * n_q + row] * kLog2e;
-          st[kRows + r] = acc;
-        }
+      acc += __shfl_xor(acc, 1);
+      acc += __shfl_xor(acc, 2);
+      acc += __shfl_xor(acc, 4);
+      if (part == 0 && ok) {
+        float *st = stats + ((size_t)h * (nq_pad / kRows) + m) * 2 * kRows;
+        st[r] = lse[(size_t)h * n_q + row] * kLog2e;
+        st[kRows + r] = acc;
       }
-      __syncthreads();
-      for (int e = tid; e < D * kRows; e += 256) {
-        const int dd = e / kRows, r = e % kRows;
-        const int64_t row = m * kRows + r;
-        if (row >= lo && row < hi) {
-          const size_t off = ((size_t)h * D + dd) * nq_pad + row;
-          qt[off] = tq[r][dd];
-          dot[off] = tdo[r][dd];
-        }
-      }
-      __syncthreads();
     }
   }
 }
@@ -176,16 +152,14 @@ __global__ __launch_bounds__(256) void zero_kernel(uint4 *__restrict__ p, int64_
 template <int D>
 struct KvShape {
   static constexpr int QC = D / 8;          // 16-byte columns of a Q / dO row
-  static constexpr int TC = kRows / 8;      // 16-byte columns of a Q^T / dO^T row (4)
   static constexpr int Q_EL = kRows * D;
-  static constexpr int T_EL = D * kRows;
   static constexpr int F_EL = 2 * 2 * kRows;                 // 64 floats as bf16 slots
-  static constexpr int STAGE_EL = 2 * Q_EL + 2 * T_EL + F_EL;
-  static constexpr int NSTAGE = 4;                            // LDS ring of query blocks
+  static constexpr int STAGE_EL = 2 * Q_EL + F_EL;
+  static constexpr int NSTAGE = 8;                            // LDS ring of query blocks
   static constexpr int NQ = kRows * QC / 64 / kWaves;   // wave loads per Q (dO) tile
-  static constexpr int NT = D * TC / 64 / kWaves;       // wave loads per Q^T (dO^T) tile
-  static constexpr int LOADS = 2 * NQ + 2 * NT;         // per wave per step (+1 on wave 0)
+  static constexpr int LOADS = 2 * NQ;                  // per wave per step (+1 on wave 0)
   static constexpr size_t SMEM = NSTAGE * STAGE_EL * sizeof(bf16);
+  static_assert((NSTAGE - 2) * (LOADS + 1) <= 63, "vmcnt range");
 };
 
 // s_waitcnt vmcnt(N) for a compile-time N.
@@ -193,12 +167,18 @@ template <int N>
 __device__ __forceinline__ void wait_vm_n() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
-// Wait until at most k * L (k = 0, 1, 2) vector-memory operations are outstanding.
-template <int L>
+// Wait until at most k * L vector-memory operations are outstanding
+// (k in [0, KMAX]; larger k wait for KMAX * L).
+template <int L, int KMAX>
 __device__ __forceinline__ void wait_stages(int k) {
-  if (k >= 2) wait_vm_n<2 * L>();
-  else if (k == 1) wait_vm_n<L>();
-  else wait_vm_n<0>();
+  bool done = false;
+  static_for<KMAX>([&](auto i) {
+    if (!done && k == int(i)) {
+      wait_vm_n<int(i) * L>();
+      done = true;
+    }
+  });
+  if (!done) wait_vm_n<KMAX * L>();
 }
 
 // Walks the steps (32-row query block x query head) that attend one KV block:
@@ -244,15 +224,42 @@ struct StepIter {
   __device__ int64_t hi() const { return (m + 1) * kRows < frb ? (m + 1) * kRows : frb; }
 };
 
+// Instruction order of one dK/dV step (one scheduling region): the S chain
+// with the Q / dO row reads, then the dP chain with the P = exp(...) VALU
+// work and the transpose reads of dO, then dV^T with the dS VALU work and the
+// transpose reads of Q, then dK^T.  With one wave per SIMD only this
+// interleaving overlaps VALU and LDS latency with the matrix cores.
+template <int NC, int NT, int VA, int VB>
+__device__ __forceinline__ void sched_kv_step() {
+  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, VA, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < NT; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, VB, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, NT, 0);
+}
+
 template <int D>
-__global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
+__global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) void attn_bwd_dkdv_kernel(
     const bf16 *__restrict__ k, const bf16 *__restrict__ v, const bf16 *__restrict__ q,
-    const bf16 *__restrict__ dout, const bf16 *__restrict__ qt, const bf16 *__restrict__ dot,
-    const float *__restrict__ stats, const int64_t *__restrict__ cu,
-    const libra_tile_t *__restrict__ tiles, int64_t T, const BwdItem *__restrict__ items,
-    int32_t *__restrict__ hdr, int h_q, int h_kv, int64_t n_q, int64_t n_kv, int64_t nq_pad,
-    float scale, float c2, void *__restrict__ dk_out, void *__restrict__ dv_out,
-    int accumulate) {
+    const bf16 *__restrict__ dout, const float *__restrict__ stats,
+    const int64_t *__restrict__ cu, const libra_tile_t *__restrict__ tiles, int64_t T,
+    const BwdItem *__restrict__ items, int32_t *__restrict__ hdr, int h_q, int h_kv,
+    int64_t n_q, int64_t n_kv, int64_t nq_pad, float scale, float c2,
+    void *__restrict__ dk_out, void *__restrict__ dv_out, int accumulate) {
   using S = KvShape<D>;
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
   __shared__ int32_t s_item;
@@ -262,21 +269,29 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
   const int G = h_q / h_kv;
   const int64_t nblk = nq_pad / kRows;
   int q_serve = blockIdx.x % kXcds, q_left = kXcds;
-  // per-lane LDS offsets (elements) of the operand reads
+  // per-lane LDS offsets (elements) of the operand reads: rows of Q / dO for
+  // S and dP (row perm32(ln), 8 columns), and the transpose reads that give
+  // dO^T / Q^T for dV^T and dK^T: this lane addresses 4 columns of row
+  // 8 kg + 4 half + i of the block (i = (l % 16) / 4), the columns whose
+  // 16-lane group hands them to the lanes that need column perm32(ln)
   const int prow = perm32(ln);
-  int qoff[D / 16], toff[2];
-  static_for<D / 16>([&](auto c) { qoff[c] = prow * D + 8 * swz<S::QC>(prow, 2 * c + kg); });
-  static_for<2>([&](auto c) { toff[c] = prow * kRows + 8 * swz<S::TC>(prow, 2 * c + kg); });
+  int qoff[D / 16], troff[D / 32][2];
+  static_for<D / 16>([&](auto c) { qoff[c] = prow * D + 8 * swt<S::QC>(prow, 2 * c + kg); });
+  {
+    const int grp = l >> 4, i = (l & 15) >> 2, r = l & 3;
+    static_for<D / 32>([&](auto dt) {
+      static_for<2>([&](auto hf) {
+        const int row = 8 * (grp >> 1) + 4 * hf + i;
+        const int chunk = 4 * dt + 2 * (grp & 1) + (r & 1);
+        troff[dt][hf] = row * D + 8 * swt<S::QC>(row, chunk) + 4 * (r >> 1);
+      });
+    });
+  }
   // per-lane parts of the staging addresses (elements), fixed for the kernel
   int q_lane[S::NQ];
-  int64_t t_lane[S::NT];
   static_for<S::NQ>([&](auto u) {
     const int r = (w + kWaves * u) * (64 / S::QC) + l / S::QC;
-    q_lane[u] = r * h_q * D + 8 * swz<S::QC>(r, l % S::QC);
-  });
-  static_for<S::NT>([&](auto u) {
-    const int r = (w + kWaves * u) * (64 / S::TC) + l / S::TC;
-    t_lane[u] = (int64_t)r * nq_pad + 8 * swz<S::TC>(r, l % S::TC);
+    q_lane[u] = r * h_q * D + 8 * swt<S::QC>(r, l % S::QC);
   });
 
   for (;;) {
@@ -307,19 +322,19 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
     });
     f32x16 dva[D / 32], dka[D / 32];
     static_for<D / 32>([&](auto dt) {
-      static_for<16>([&](auto r) { dva[dt][int(r)] = 0.f; dka[dt][int(r)] = 0.f; });
+      dva[dt] = mfma_zero();
+      dka[dt] = mfma_zero();
     });
 
-    // ---- one step = (32-row query block, head); its Q, dO, Q^T, dO^T and
-    // stats go global -> LDS into ring stage `sg` (rows of the block outside
-    // the fragment are masked in the compute; Q^T / dO^T hold zeros there)
+    // ---- one step = (32-row query block, head); its Q, dO rows and stats go
+    // global -> LDS into ring stage `sg` (rows of the block outside the
+    // fragment are real rows of other fragments or the clamped last row;
+    // their P and dS are masked to zero)
     auto issue = [&](const StepIter &st, int sg) {
       const int64_t m0 = st.m * kRows;
       bf16 *Qs = smem + sg * S::STAGE_EL;
       bf16 *dOs = Qs + S::Q_EL;
-      bf16 *Qts = dOs + S::Q_EL;
-      bf16 *dOts = Qts + S::T_EL;
-      bf16 *Fs = dOts + S::T_EL;
+      bf16 *Fs = dOs + S::Q_EL;
       if (m0 + kRows <= n_q) {
         const size_t qbase = ((size_t)m0 * h_q + st.h) * D;
         static_for<S::NQ>([&](auto u) {
@@ -333,18 +348,109 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
           const int wl = w + kWaves * u;
           const int r = wl * (64 / S::QC) + l / S::QC;
           const int64_t row = m0 + r < n_q ? m0 + r : n_q - 1;
-          const size_t off = ((size_t)row * h_q + st.h) * D + 8 * swz<S::QC>(r, l % S::QC);
+          const size_t off = ((size_t)row * h_q + st.h) * D + 8 * swt<S::QC>(r, l % S::QC);
           g2l16(q + off, Qs + wl * 512);
           g2l16(dout + off, dOs + wl * 512);
         });
       }
-      const size_t tbase = (size_t)st.h * D * nq_pad + m0;
-      static_for<S::NT>([&](auto u) {
-        const int wl = w + kWaves * u;
-        g2l16(qt + tbase + t_lane[u], Qts + wl * 512);
-        g2l16(dot + tbase + t_lane[u], dOts + wl * 512);
-      });
       if (w == 0 && l < 16) g2l16(stats + ((size_t)st.h * nblk + st.m) * 64 + 4 * l, Fs);
+    };
+
+    // ---- compute one step from the LDS stage at Qs.  Rows of the block are
+    // m0 + iq, iq in [0, 32); with MASK, row iq counts for this lane's key
+    // only when lower <= iq < upper (inside the fragment and causal).
+    auto step = [&](bool full, const bf16 *Qs, int lower, int upper) {
+      constexpr int NC = D / 16, NT = D / 32;
+      const bf16 *dOs = Qs + S::Q_EL;
+      const float *l2s = reinterpret_cast<const float *>(dOs + S::Q_EL);
+      const float *dvs = l2s + kRows;
+      // (1) Q rows and the LSE values of this lane's rows
+      bf16x8 qa[NC], oa[NC];
+      f32x4 l2v[4], ddv[4];
+      static_for<NC>([&](auto c) { qa[c] = *reinterpret_cast<const bf16x8 *>(Qs + qoff[c]); });
+      static_for<4>([&](auto j) {
+        l2v[j] = *reinterpret_cast<const f32x4 *>(l2s + 16 * (j >> 1) + 8 * kg + 4 * (j & 1));
+      });
+      __builtin_amdgcn_sched_barrier(0);
+      // (2) S = Q K^T (queries on M, this lane's key on N) while dO rows and
+      // the D values load
+      f32x16 sa = mfma_zero_c(), pa;
+      static_for<NC>([&](auto c) { sa = mfma32(qa[c], kf[c], sa); });
+      static_for<NC>([&](auto c) { oa[c] = *reinterpret_cast<const bf16x8 *>(dOs + qoff[c]); });
+      static_for<4>([&](auto j) {
+        ddv[j] = *reinterpret_cast<const f32x4 *>(dvs + 16 * (j >> 1) + 8 * kg + 4 * (j & 1));
+      });
+      static_for<NC>([&](auto i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, i < 6 ? 2 : 0, 0);
+      });
+      __builtin_amdgcn_sched_barrier(0);
+      // (3) dP = dO V^T with P = exp2(S c2 - LSE log2 e) on the VALU and the
+      // transpose reads of dO^T; register 8 hh + i of S holds row 16 hh + 8 kg + i
+      bf16x8 ta[NT][2];
+      float pf[16];
+      bf16x8 pb16[2], db16[2];
+      auto phase3 = [&](auto mask_t) {
+      constexpr bool MASK = decltype(mask_t)::value;
+      pa = mfma_zero_c();
+      static_for<NC>([&](auto c) { pa = mfma32(oa[c], vf[c], pa); });
+      static_for<2>([&](auto hh) {
+        static_for<8>([&](auto i) {
+          constexpr int r = 8 * hh + i;
+          const float l2 = l2v[2 * hh + (i >> 2)][int(i) & 3];
+          float p = fast_exp2(__builtin_fmaf(sa[r], c2, -l2));
+          if constexpr (MASK) {
+            const int iq = 16 * hh + 8 * kg + i;
+            p = (iq >= lower && iq < upper) ? p : 0.f;
+          }
+          pf[r] = p;
+          pb16[hh][int(i)] = static_cast<bf16>(p);
+        });
+      });
+      static_for<NT>([&](auto dt) {
+        static_for<2>([&](auto c) {
+          const bf16 *base = dOs + 16 * c * D;
+          ta[dt][c] = lds_tr16x2(base + troff[dt][0], base + troff[dt][1]);
+        });
+      });
+      static_for<NC>([&](auto i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, MASK ? 10 : 7, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      });
+      };
+      if (full) phase3(std::false_type{});
+      else phase3(std::true_type{});
+      __builtin_amdgcn_sched_barrier(0);
+      // (4) dV^T += dO^T P with dS = P (dP - D) on the VALU and the transpose
+      // reads of Q^T
+      bf16x8 tq[NT][2];
+      static_for<NT>([&](auto dt) {
+        static_for<2>([&](auto c) { dva[dt] = mfma32(ta[dt][c], pb16[c], dva[dt]); });
+      });
+      static_for<2>([&](auto hh) {
+        static_for<8>([&](auto i) {
+          constexpr int r = 8 * hh + i;
+          const float dd = ddv[2 * hh + (i >> 2)][int(i) & 3];
+          db16[hh][int(i)] = static_cast<bf16>(pf[r] * (pa[r] - dd));
+        });
+      });
+      static_for<NT>([&](auto dt) {
+        static_for<2>([&](auto c) {
+          const bf16 *base = Qs + 16 * c * D;
+          tq[dt][c] = lds_tr16x2(base + troff[dt][0], base + troff[dt][1]);
+        });
+      });
+      static_for<2 * NT>([&](auto i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 7, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      });
+      __builtin_amdgcn_sched_barrier(0);
+      // (5) dK^T += Q^T dS
+      static_for<NT>([&](auto dt) {
+        static_for<2>([&](auto c) { dka[dt] = mfma32(tq[dt][c], db16[c], dka[dt]); });
+      });
     };
 
     StepIter iss{tiles, T, n_q, n_kv, key0, len, h_q, g, G, kloc0};
@@ -352,72 +458,28 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
     StepIter cur = iss;
     int issued = 0, computed = 0;
     while (cur.valid) {
-      // keep up to two steps in flight beyond the one computed now
+      // keep up to NSTAGE - 1 steps in flight, the one computed now included
       while (iss.valid && issued < computed + S::NSTAGE - 1) {
         issue(iss, issued % S::NSTAGE);
         iss.next();
         ++issued;
       }
       const int after = issued - 1 - computed;          // steps issued after this one
-      if (w == 0) wait_stages<S::LOADS + 1>(after); else wait_stages<S::LOADS>(after);
+      if (w == 0) wait_stages<S::LOADS + 1, S::NSTAGE - 2>(after);
+      else wait_stages<S::LOADS, S::NSTAGE - 2>(after);
       __syncthreads();
 
-      // ---- compute the step from ring stage computed % NSTAGE
-      // rows of the block are m0 + iq, iq in [0, 32); row iq is valid for this
-      // lane's key when lower <= iq < upper (inside the fragment and causal).
       const int64_t m0 = cur.m * kRows;
       const int lo_l = (int)(cur.lo() - m0), hi_l = (int)(cur.hi() - m0);
       const int64_t qb = cur.qla + (m0 - cur.fra);            // q_loc of row m0
       if ((int64_t)kw0 <= qb + hi_l - 1) {
         const bf16 *Qs = smem + (computed % S::NSTAGE) * S::STAGE_EL;
-        const bf16 *dOs = Qs + S::Q_EL;
-        const bf16 *Qts = dOs + S::Q_EL;
-        const bf16 *dOts = Qts + S::T_EL;
-        const float *l2s = reinterpret_cast<const float *>(dOts + S::T_EL);
-        const float *dvs = l2s + kRows;
-        f32x16 sa, pa;
-        static_for<16>([&](auto r) { sa[int(r)] = 0.f; pa[int(r)] = 0.f; });
-        static_for<D / 16>([&](auto c) {
-          sa = mfma32(*reinterpret_cast<const bf16x8 *>(Qs + qoff[c]), kf[c], sa);
-          pa = mfma32(*reinterpret_cast<const bf16x8 *>(dOs + qoff[c]), vf[c], pa);
-        });
-        // keep the LDS reads a few MFMAs ahead (one wave per SIMD: nothing
-        // else hides their latency)
-        sched_pipeline<2 * (D / 16), 4>();
         // interior blocks: every row inside the fragment and at or after every key
         const bool full = lo_l == 0 && hi_l == kRows && wave_keys_ok && kw0 + 31 <= qb;
         const int64_t need = (int64_t)kl - qb;                // first iq with q_loc >= kl
-        const int lower = full ? 0 : (int)(need > lo_l ? (need < kRows ? need : kRows) : lo_l);
-        const int upper = full ? kRows : (key_ok ? hi_l : 0);
-        bf16x8 pb16[2], db16[2];
-        static_for<2>([&](auto hh) {
-          const int iq0 = 16 * hh + 8 * kg;
-          const f32x4 la = *reinterpret_cast<const f32x4 *>(l2s + iq0);
-          const f32x4 lb = *reinterpret_cast<const f32x4 *>(l2s + iq0 + 4);
-          const f32x4 da = *reinterpret_cast<const f32x4 *>(dvs + iq0);
-          const f32x4 db = *reinterpret_cast<const f32x4 *>(dvs + iq0 + 4);
-          static_for<8>([&](auto i) {
-            constexpr int r = 8 * hh + i;
-            const float l2 = i < 4 ? la[int(i) & 3] : lb[int(i) & 3];
-            const float dd = i < 4 ? da[int(i) & 3] : db[int(i) & 3];
-            float p = fast_exp2(__builtin_fmaf(sa[r], c2, -l2));
-            if (!full) {
-              const int iq = iq0 + i;
-              p = (iq >= lower && iq < upper) ? p : 0.f;
-            }
-            pb16[hh][int(i)] = static_cast<bf16>(p);
-            db16[hh][int(i)] = static_cast<bf16>(p * (pa[r] - dd));
-          });
-        });
-        static_for<D / 32>([&](auto dt) {
-          const bf16 *ap = dOts + 32 * dt * kRows;
-          const bf16 *bp = Qts + 32 * dt * kRows;
-          static_for<2>([&](auto c) {
-            dva[dt] = mfma32(*reinterpret_cast<const bf16x8 *>(ap + toff[c]), pb16[c], dva[dt]);
-            dka[dt] = mfma32(*reinterpret_cast<const bf16x8 *>(bp + toff[c]), db16[c], dka[dt]);
-          });
-        });
-        sched_pipeline<4 * (D / 32), 4>();
+        const int lower = (int)(need > lo_l ? (need < kRows ? need : kRows) : lo_l);
+        const int upper = key_ok ? hi_l : 0;
+        step(full, Qs, lower, upper);
       }
       ++computed;
       cur.next();
@@ -635,9 +697,7 @@ BwdLayout bwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, i
   L.items = align256b(L.gmask + (size_t)n * sizeof(unsigned long long));
   L.qitems = align256b(L.items + (size_t)L.max_items * sizeof(BwdItem));
   L.stats = align256b(L.qitems + (size_t)L.max_qitems * sizeof(FwdItem));
-  L.qt = align256b(L.stats + (size_t)h_q * L.nq_pad * 2 * sizeof(float));
-  L.dot = align256b(L.qt + (size_t)h_q * d * L.nq_pad * sizeof(bf16));
-  L.kt = align256b(L.dot + (size_t)h_q * d * L.nq_pad * sizeof(bf16));
+  L.kt = align256b(L.stats + (size_t)h_q * L.nq_pad * 2 * sizeof(float));
   L.total = align256b(L.kt + (size_t)h_kv * d * L.pitch * sizeof(bf16));
   return L;
 }
@@ -655,8 +715,6 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
   BwdItem *items = reinterpret_cast<BwdItem *>(ws + L.items);
   FwdItem *qitems = reinterpret_cast<FwdItem *>(ws + L.qitems);
   float *stats = reinterpret_cast<float *>(ws + L.stats);
-  bf16 *qt = reinterpret_cast<bf16 *>(ws + L.qt);
-  bf16 *dot = reinterpret_cast<bf16 *>(ws + L.dot);
   bf16 *kt = reinterpret_cast<bf16 *>(ws + L.kt);
   static bool attr_set = false;
   if (!attr_set) {
@@ -680,27 +738,21 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
                        h_kv, n_q, n_kv, hdr, ext, gmask, items, L.max_items);
     enqueue_fwd_items(cu, n, tiles, T, h_q, h_kv, n_q, n_kv, hdr, qitems, L.max_qitems, st);
     {
-      // Q^T / dO^T (and the stats) are zero outside the covered rows: query
-      // blocks of the dK/dV kernel contract over all 32 rows of a block
-      const int64_t n16 = (int64_t)h_q * D * L.nq_pad * (int64_t)sizeof(bf16) / 16;
-      const unsigned blocks = (unsigned)std::min<int64_t>((n16 + 255) / 256, 4096);
-      hipLaunchKernelGGL(zero_kernel, dim3(blocks), dim3(256), 0, st, reinterpret_cast<uint4 *>(qt),
-                         n16);
-      hipLaunchKernelGGL(zero_kernel, dim3(blocks), dim3(256), 0, st,
-                         reinterpret_cast<uint4 *>(dot), n16);
+      // stats of rows outside the covered ones stay zero (finite): they are
+      // only read for masked rows
       const int64_t s16 = (int64_t)h_q * L.nq_pad * 2 * (int64_t)sizeof(float) / 16;
       hipLaunchKernelGGL(zero_kernel, dim3((unsigned)std::min<int64_t>((s16 + 255) / 256, 4096)),
                          dim3(256), 0, st, reinterpret_cast<uint4 *>(stats), s16);
     }
-    hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)(T * kTileSplit)), dim3(256), 0, st, q, o,
-                       dout, lse, tiles, h_q, n_q, n_kv, L.nq_pad, stats, qt, dot);
+    hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)(T * kTileSplit)), dim3(256), 0, st, o,
+                       dout, lse, tiles, h_q, n_q, n_kv, L.nq_pad, stats);
     enqueue_transpose(k, cu, n, n_kv, h_kv, D, L.pitch, kt, st);
     int dev = 0, cus = 256;
     hipGetDevice(&dev);
     hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (tm_kv) hipEventRecord(tm_kv->begin, st);
     hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(cus), dim3(kThreads), KvShape<D>::SMEM, st, k,
-                       v, q, dout, qt, dot, stats, cu, tiles, T, items, hdr, h_q, h_kv, n_q, n_kv,
+                       v, q, dout, stats, cu, tiles, T, items, hdr, h_q, h_kv, n_q, n_kv,
                        L.nq_pad, scale, scale * kLog2e, dk, dv, accumulate ? 1 : 0);
     if (tm_kv) hipEventRecord(tm_kv->end, st);
     if (tm_q) hipEventRecord(tm_q->begin, st);

@@ -12,6 +12,8 @@ namespace libra {
 
 typedef __bf16 bf16;
 typedef bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -155,6 +157,26 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// acc += A B with the accumulator pinned to AGPRs (inline asm: the compiler's
+// MFMA form is chosen per function, and kernels whose long-lived
+// accumulators must not occupy the 256 architectural VGPRs use this one).
+// The two leading wait states cover a VALU write of A or B or of the
+// accumulator (zero-initialisation) immediately before.  Reading acc with
+// VALU or memory instructions afterwards needs mfma_acc_drain first.
+__device__ __forceinline__ void mfma32_agpr(f32x16 &acc, bf16x8 a, bf16x8 b) {
+  asm("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+// acc = 0 in AGPRs (an MFMA of zero operands with a zero accumulator), so that
+// the accumulator never lives in VGPRs.
+__device__ __forceinline__ void mfma_agpr_zero(f32x16 &acc) {
+  const bf16x8 z = {};
+  asm("v_mfma_f32_32x32x16_bf16 %0, %1, %1, 0" : "=a"(acc) : "v"(z));
+}
+// Wait states between the last mfma32_agpr into acc and any other read of it.
+__device__ __forceinline__ void mfma_acc_drain(f32x16 &a0, f32x16 &a1) {
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3" : "+a"(a0), "+a"(a1));
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // LDS tiles are stored without padding; the 16-byte column of a row is
@@ -164,6 +186,39 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 template <int C>
 __device__ __forceinline__ int swz(int row, int col) {
   return col ^ ((row / (16 / C)) & (C - 1));
+}
+
+// Swizzle of row-major Q / dO / K / V tiles that are read both by rows
+// (16-byte reads, 16 consecutive rows per pass) and by the LDS transpose
+// reads below (8-byte reads of 4 rows x 64 bytes per pass, rows 4j..4j+3).
+// The chunk is XORed with a bit rotation of the row that spreads either
+// pattern over all 64 banks.  C = 16-byte columns per row (8 or 16).
+template <int C>
+__host__ __device__ __forceinline__ int swt(int row, int col) {
+  static_assert(C == 8 || C == 16, "tiles of 64 or 128 bf16 per row");
+  if constexpr (C == 16) {
+    const int x = row & 15;
+    return col ^ (((x & 3) << 2) | (x >> 2));
+  } else {
+    const int x = (row >> 1) & 7;
+    return col ^ (((x & 1) << 2) | (x >> 1));
+  }
+}
+
+// gfx950 LDS transpose read (ds_read_b64_tr_b16).  Within each group of 16
+// lanes, lane 4r + e receives as element i the 16-bit element e of the
+// 8 bytes addressed by lane 4i + r of the same group: 16 lanes that address
+// 4 consecutive elements of 4 rows each come back holding one column of 4
+// rows each, i.e. a 4 x 16 block read transposed.
+__device__ __forceinline__ bf16x4 lds_tr16(const bf16 *p) {
+  const i16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4 *)(p));
+  return __builtin_bit_cast(bf16x4, r);
+}
+// An MFMA operand of 8 consecutive rows at one column from two transpose reads.
+__device__ __forceinline__ bf16x8 lds_tr16x2(const bf16 *p0, const bf16 *p1) {
+  const bf16x4 a = lds_tr16(p0), b = lds_tr16(p1);
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
 // Asynchronous 16-byte global -> LDS copy by one wave: lane i's bytes land at
@@ -203,6 +258,26 @@ __device__ __forceinline__ void static_for(F &&f) {
   static_for_impl<0, N>(f);
 }
 
+// A zero accumulator produced by an MFMA: in kernels whose MFMAs write
+// AGPRs this keeps long-lived accumulators in AGPRs from their first
+// definition (a VALU zero-fill would be a VGPR definition and make the
+// register allocator copy the accumulators between the two files).
+__device__ __forceinline__ f32x16 mfma_zero() {
+  bf16x8 z;
+  static_for<8>([&](auto i) { z[int(i)] = bf16(0.f); });
+  f32x16 c;
+  static_for<16>([&](auto i) { c[int(i)] = 0.f; });
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(z, z, c, 0, 0, 0);
+}
+
+// A zero accumulator as a plain constant (the first MFMA of a chain reads it
+// as the inline constant 0).
+__device__ __forceinline__ f32x16 mfma_zero_c() {
+  f32x16 c;
+  static_for<16>([&](auto i) { c[int(i)] = 0.f; });
+  return c;
+}
+
 // First index i in [0, n] with a[i] > x (a sorted ascending, n+1 entries read at most n).
 __device__ __forceinline__ int64_t upper_bound64(const int64_t *a, int64_t n, int64_t x) {
   int64_t lo = 0, hi = n;
@@ -228,7 +303,7 @@ struct FwdLayout {
   int64_t max_items = 0, pitch = 0;
 };
 struct BwdLayout {
-  size_t hdr = 0, ext = 0, gmask = 0, items = 0, qitems = 0, stats = 0, qt = 0, dot = 0, kt = 0,
+  size_t hdr = 0, ext = 0, gmask = 0, items = 0, qitems = 0, stats = 0, kt = 0,
          total = 0;
   int64_t max_items = 0, max_qitems = 0, nq_pad = 0, pitch = 0;
 };
