@@ -467,7 +467,7 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
       const int after = issued - 1 - computed;          // steps issued after this one
       if (w == 0) wait_stages<S::LOADS + 1, S::NSTAGE - 2>(after);
       else wait_stages<S::LOADS, S::NSTAGE - 2>(after);
-      __syncthreads();
+      barrier_nofence();
 
       const int64_t m0 = cur.m * kRows;
       const int lo_l = (int)(cur.lo() - m0), hi_l = (int)(cur.hi() - m0);

@@ -226,6 +226,12 @@ __device__ __forceinline__ bf16x8 lds_tr16x2(const bf16 *p0, const bf16 *p1) {
 __device__ __forceinline__ void g2l16(const void *g, bf16 *lds) {
   __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void *)lds, 16, 0, 0);
 }
+// Workgroup barrier without the memory fence of __syncthreads(): the fence
+// would wait for every outstanding global load of the wave, including the
+// global -> LDS prefetches of later pipeline stages.  Callers make the data
+// they publish complete first (s_waitcnt on the loads that filled it).
+__device__ __forceinline__ void barrier_nofence() { __builtin_amdgcn_s_barrier(); }
+
 // Wait for this wave's outstanding global loads (including global -> LDS).
 __device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
