@@ -30,14 +30,22 @@ def _hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def hip_flags():
+# Per-source extra flags.  The forward kernel keeps its MFMA accumulators in
+# VGPRs (two workgroups per CU; the default heuristic shuffles them through
+# AGPRs inside the hot loop).  The backward kernels keep the long-lived dK /
+# dV / dQ accumulators in AGPRs, which is the default form once they are
+# initialised by an MFMA, and leaves the 256 VGPRs to the operands in flight.
+EXTRA_FLAGS = {
+    "attn_fwd.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1"],
+    "attn_api.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1"],
+}
+
+
+def hip_flags(src: str = ""):
     return [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-munsafe-fp-atomics",
             # no packed-fp32 instructions anywhere in the device code
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-            # MFMA accumulators in VGPRs: the default heuristic shuffles them
-            # through AGPRs inside the hot loops of the occupancy-1 kernels
-            "-mllvm", "--amdgpu-mfma-vgpr-form=1",
-            f"-I{INCLUDE}", f"-I{CSRC}"]
+            f"-I{INCLUDE}", f"-I{CSRC}"] + EXTRA_FLAGS.get(src, [])
 
 
 def _run(cmd, verbose):
@@ -62,7 +70,7 @@ def build(verbose: bool = False, jobs: int = 4) -> str:
         objs.append(obj)
     for src in HIP_SOURCES:
         obj = os.path.join(OUT_DIR, src + ".o")
-        cmds.append([hipcc] + hip_flags() + ["-c", os.path.join(CSRC, src), "-o", obj])
+        cmds.append([hipcc] + hip_flags(src) + ["-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
     procs = []
     for cmd in cmds:

@@ -17,12 +17,13 @@
 //     staged in an LDS ring, up to seven ahead of the one computed.
 //   * dQ, query-stationary, shaped like the forward: S^T = K Q^T and
 //     dP^T = V dO^T (lane = query), dS^T = P^T * (dP^T - D), then
-//     dQ^T += K^T dS^T.  It recomputes S and dP instead of accumulating dQ
+//     dQ^T += K^T dS^T; key blocks are staged in a 4-deep LDS ring.  It recomputes S and dP instead of accumulating dQ
 //     across key blocks with atomics: on long samples that accumulation is
 //     read-modify-write traffic of 4 bytes x d per (32 queries x 128 keys)
 //     per head, which would bound the whole backward by HBM.
-// Preparation: D = rowsum(dO * O), a padded transposed K^T for the dQ
-// kernel, plus the two work-item lists, longest first.
+// Preparation: D = rowsum(dO * O) and the two work-item lists, longest
+// first.  Every transposed operand (dO^T, Q^T, K^T) is read from row-major
+// LDS tiles with the LDS transpose reads.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -526,32 +527,50 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
 template <int D>
 struct DqShape {
   static constexpr int KC = D / 8;            // 16-byte columns of a K / V row
-  static constexpr int TC = kFwdBN / 8;       // 16-byte columns of a K^T row
   static constexpr int K_EL = kFwdBN * D;
-  static constexpr int T_EL = D * kFwdBN;
-  static constexpr int STAGE = 2 * K_EL + T_EL;
-  static constexpr int NK = kFwdBN * KC / 64 / kWaves;
-  static constexpr int NT = D * TC / 64 / kWaves;
-  static constexpr size_t SMEM = 2 * STAGE * sizeof(bf16);
+  static constexpr int STAGE = 2 * K_EL;
+  static constexpr int NSTAGE = 4;            // LDS ring of key blocks
+  static constexpr int NK = kFwdBN * KC / 64 / kWaves;   // wave loads per K (V) tile
+  static constexpr int LOADS = 2 * NK;                    // per wave per block
+  static constexpr size_t SMEM = NSTAGE * STAGE * sizeof(bf16);
+  static_assert((NSTAGE - 1) * LOADS <= 63, "vmcnt range");
 };
 
 template <int D>
 __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
     const bf16 *__restrict__ q, const bf16 *__restrict__ dout, const bf16 *__restrict__ k,
-    const bf16 *__restrict__ v, const bf16 *__restrict__ kt, const float *__restrict__ stats,
+    const bf16 *__restrict__ v, const float *__restrict__ stats,
     const int64_t *__restrict__ cu, const FwdItem *__restrict__ items,
     int32_t *__restrict__ hdr, int h_q, int h_kv, int64_t n_q, int64_t n_kv, int64_t nq_pad,
-    int64_t pitch, float c2, float scale, bf16 *__restrict__ dq) {
+    float c2, float scale, bf16 *__restrict__ dq) {
   using S = DqShape<D>;
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
   __shared__ int32_t s_item;
   const int tid = threadIdx.x, l = tid & 63, ln = l & 31, kg = l >> 5;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
   int q_serve = blockIdx.x % kXcds, q_left = kXcds;
+  // per-lane LDS offsets (elements): K / V rows perm32(ln) for S^T and dP^T,
+  // and the transpose reads of the K tile that give the K^T operand of dQ^T
+  // (as in the dK/dV kernel, with keys in place of query rows)
   const int prow = perm32(ln);
-  int koff[D / 16], toff_l[4];
-  static_for<D / 16>([&](auto c) { koff[c] = prow * D + 8 * swz<S::KC>(prow, 2 * c + kg); });
-  static_for<4>([&](auto c) { toff_l[c] = prow * kFwdBN + 8 * swz<S::TC>(prow, 2 * c + kg); });
+  int koff[D / 16], troff[D / 32][2];
+  static_for<D / 16>([&](auto c) { koff[c] = prow * D + 8 * swt<S::KC>(prow, 2 * c + kg); });
+  {
+    const int grp = l >> 4, i = (l & 15) >> 2, r = l & 3;
+    static_for<D / 32>([&](auto dt) {
+      static_for<2>([&](auto hf) {
+        const int row = 8 * (grp >> 1) + 4 * hf + i;
+        const int chunk = 4 * dt + 2 * (grp & 1) + (r & 1);
+        troff[dt][hf] = row * D + 8 * swt<S::KC>(row, chunk) + 4 * (r >> 1);
+      });
+    });
+  }
+  // staging: wave load u covers rows (w + 4u) * 64 / KC + l / KC of a tile
+  int kst[S::NK];
+  static_for<S::NK>([&](auto u) {
+    const int r = (w + kWaves * u) * (64 / S::KC) + l / S::KC;
+    kst[u] = r;
+  });
 
   for (;;) {
     if (tid == 0) s_item = take_item(hdr, kFwdQ, q_serve, q_left);
@@ -560,7 +579,6 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
     if (idx < 0) break;
     const FwdItem it = items[idx];
     const int64_t key0 = cu[it.sample];
-    const int64_t toff = vt_offset(key0, it.sample);
     const int head = it.head0 + (w % it.nh);
     const int wrow0 = (w / it.nh) * kRows;
     const int wrows = min(max(it.nrows - wrow0, 0), kRows);
@@ -586,47 +604,39 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
       dd_q = st[kRows + row % kRows];
     }
     f32x16 acc[D / 32];
-#pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[dt][r] = 0.f;
+    static_for<D / 32>([&](auto dt) { acc[dt] = mfma_zero(); });
 
-    // global -> LDS, asynchronous: K and V rows of block b (keys past the
-    // buffer read the last key instead; they are masked) and the K^T block
-    // of the padded transposed copy
-    auto issue = [&](int b, int buf) {
-      bf16 *Ks = smem + buf * S::STAGE;
+    // global -> LDS, asynchronous: K and V rows of key block b (keys past the
+    // buffer read the last key instead; they are masked)
+    auto issue = [&](int b, int sg) {
+      bf16 *Ks = smem + sg * S::STAGE;
       bf16 *Vs = Ks + S::K_EL;
-      bf16 *Ts = Vs + S::K_EL;
       static_for<S::NK>([&](auto u) {
         const int wl = w + kWaves * u;
-        const int r = wl * (64 / S::KC) + l / S::KC;
-        const int col = swz<S::KC>(r, l % S::KC);
+        const int r = kst[u];
         int64_t key = key0 + (int64_t)b * kFwdBN + r;
         key = key < n_kv ? key : n_kv - 1;
-        const size_t off = ((size_t)key * h_kv + it.g) * D + 8 * col;
+        const size_t off = ((size_t)key * h_kv + it.g) * D + 8 * swt<S::KC>(r, l % S::KC);
         g2l16(k + off, Ks + wl * 512);
         g2l16(v + off, Vs + wl * 512);
       });
-      static_for<S::NT>([&](auto u) {
-        const int wl = w + kWaves * u;
-        const int r = wl * (64 / S::TC) + l / S::TC;
-        const int col = swz<S::TC>(r, l % S::TC);
-        g2l16(kt + ((size_t)it.g * D + r) * pitch + toff + (int64_t)b * kFwdBN + 8 * col,
-              Ts + wl * 512);
-      });
     };
 
-    issue(0, 0);
-    wait_vm();
-    __syncthreads();
+    int issued = 0;
+    for (; issued < nkb && issued < S::NSTAGE - 1; ++issued) issue(issued, issued);
     for (int b = 0; b < nkb; ++b) {
-      const int buf = b & 1;
-      if (b + 1 < nkb) issue(b + 1, buf ^ 1);
+      // this block's loads are complete once at most (issued - 1 - b) later
+      // blocks are outstanding; then every wave's part is in LDS
+      wait_stages<S::LOADS, S::NSTAGE - 2>(issued - 1 - b);
+      barrier_nofence();
+      // the stage of block b - 1 is free again (every wave passed the barrier)
+      if (issued < nkb) {
+        issue(issued, issued % S::NSTAGE);
+        ++issued;
+      }
       if (b < wave_nkb) {
-        const bf16 *Ks = smem + buf * S::STAGE;
+        const bf16 *Ks = smem + (b % S::NSTAGE) * S::STAGE;
         const bf16 *Vs = Ks + S::K_EL;
-        const bf16 *Ts = Vs + S::K_EL;
         f32x16 s[2], dp[2];
         static_for<2>([&](auto t) {
           static_for<16>([&](auto r) { s[t][int(r)] = 0.f; dp[t][int(r)] = 0.f; });
@@ -655,17 +665,19 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
             dsf[2 * t + (r >> 3)][r & 7] = static_cast<bf16>(p * (dp[t][int(r)] - dd_q));
           });
         });
+        // dQ^T += K^T dS^T; key chunk c = 16 keys from tile row 16 c
         static_for<D / 32>([&](auto dt) {
           static_for<4>([&](auto c) {
-            acc[dt] = mfma32(*reinterpret_cast<const bf16x8 *>(Ts + 32 * dt * kFwdBN + toff_l[c]),
-                             dsf[c], acc[dt]);
+            const bf16 *base = Ks + 16 * c * D;
+            acc[dt] = mfma32(lds_tr16x2(base + troff[dt][0], base + troff[dt][1]), dsf[c],
+                             acc[dt]);
           });
         });
         sched_pipeline<4 * (D / 32), 4>();
       }
-      wait_vm();
-      __syncthreads();
     }
+    wait_vm_n<0>();
+    __syncthreads();   // the ring is reused by the next item
 
     if (active && ln < wrows) {
       bf16 *op = dq + ((size_t)row * h_q + head) * D + 8 * kg;
@@ -690,15 +702,13 @@ BwdLayout bwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, i
   L.max_items = (n_kv / kBwdBK + n + 1) * (int64_t)h_kv;
   L.max_qitems = fwd_max_items(T, n, n_q, h_q, h_kv);
   L.nq_pad = (n_q + kRows - 1) / kRows * kRows;
-  L.pitch = vt_pitch(n_kv, n);
   L.hdr = 0;
   L.ext = align256b(kHdrSlots * sizeof(int32_t));
   L.gmask = align256b(L.ext + (size_t)n * sizeof(int32_t));
   L.items = align256b(L.gmask + (size_t)n * sizeof(unsigned long long));
   L.qitems = align256b(L.items + (size_t)L.max_items * sizeof(BwdItem));
   L.stats = align256b(L.qitems + (size_t)L.max_qitems * sizeof(FwdItem));
-  L.kt = align256b(L.stats + (size_t)h_q * L.nq_pad * 2 * sizeof(float));
-  L.total = align256b(L.kt + (size_t)h_kv * d * L.pitch * sizeof(bf16));
+  L.total = align256b(L.stats + (size_t)h_q * L.nq_pad * 2 * sizeof(float));
   return L;
 }
 
@@ -715,7 +725,6 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
   BwdItem *items = reinterpret_cast<BwdItem *>(ws + L.items);
   FwdItem *qitems = reinterpret_cast<FwdItem *>(ws + L.qitems);
   float *stats = reinterpret_cast<float *>(ws + L.stats);
-  bf16 *kt = reinterpret_cast<bf16 *>(ws + L.kt);
   static bool attr_set = false;
   if (!attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_bwd_dkdv_kernel<D>),
@@ -746,7 +755,6 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
     }
     hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)(T * kTileSplit)), dim3(256), 0, st, o,
                        dout, lse, tiles, h_q, n_q, n_kv, L.nq_pad, stats);
-    enqueue_transpose(k, cu, n, n_kv, h_kv, D, L.pitch, kt, st);
     int dev = 0, cus = 256;
     hipGetDevice(&dev);
     hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
@@ -757,8 +765,8 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
     if (tm_kv) hipEventRecord(tm_kv->end, st);
     if (tm_q) hipEventRecord(tm_q->begin, st);
     hipLaunchKernelGGL(attn_bwd_dq_kernel<D>, dim3(cus), dim3(kThreads), DqShape<D>::SMEM, st, q,
-                       dout, k, v, kt, stats, cu, qitems, hdr, h_q, h_kv, n_q, n_kv, L.nq_pad,
-                       L.pitch, scale * kLog2e, scale, dq);
+                       dout, k, v, stats, cu, qitems, hdr, h_q, h_kv, n_q, n_kv, L.nq_pad,
+                       scale * kLog2e, scale, dq);
     if (tm_q) hipEventRecord(tm_q->end, st);
   }
   const hipError_t e = hipGetLastError();

@@ -309,9 +309,8 @@ struct FwdLayout {
   int64_t max_items = 0, pitch = 0;
 };
 struct BwdLayout {
-  size_t hdr = 0, ext = 0, gmask = 0, items = 0, qitems = 0, stats = 0, kt = 0,
-         total = 0;
-  int64_t max_items = 0, max_qitems = 0, nq_pad = 0, pitch = 0;
+  size_t hdr = 0, ext = 0, gmask = 0, items = 0, qitems = 0, stats = 0, total = 0;
+  int64_t max_items = 0, max_qitems = 0, nq_pad = 0;
 };
 
 FwdLayout fwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, int h_kv, int d);
