@@ -321,6 +321,7 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
         static_for<8>([&](auto i) { kf[c][int(i)] = bf16(0.f); vf[c][int(i)] = bf16(0.f); });
       }
     });
+    wait_vm_known();
     f32x16 dva[D / 32], dka[D / 32];
     static_for<D / 32>([&](auto dt) {
       dva[dt] = mfma_zero();
@@ -603,6 +604,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
       l2 = st[row % kRows];
       dd_q = st[kRows + row % kRows];
     }
+    wait_vm_known();
     f32x16 acc[D / 32];
     static_for<D / 32>([&](auto dt) { acc[dt] = mfma_zero(); });
 

@@ -223,14 +223,38 @@ __device__ __forceinline__ bf16x8 lds_tr16x2(const bf16 *p0, const bf16 *p1) {
 
 // Asynchronous 16-byte global -> LDS copy by one wave: lane i's bytes land at
 // lds + 16 * i; `lds` must be the same for every lane of the wave.
+//
+// Written as inline asm on purpose: for the builtin the compiler tracks the
+// asynchronous LDS write and, unable to tell ring stages apart, waits for
+// every outstanding global -> LDS load (vmcnt(0)) before the first LDS read
+// that follows, which defeats a multi-stage ring.  Callers wait for their own
+// stages (s_waitcnt vmcnt(N)) before reading them.  M0 (the LDS destination
+// of the instruction) is saved and restored around it.
 __device__ __forceinline__ void g2l16(const void *g, bf16 *lds) {
-  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void *)lds, 16, 0, 0);
+  const uint32_t a = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(size_t)(__attribute__((address_space(3))) bf16 *)lds);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(g), "s"(a)
+      : "memory");
 }
 // Workgroup barrier without the memory fence of __syncthreads(): the fence
 // would wait for every outstanding global load of the wave, including the
 // global -> LDS prefetches of later pipeline stages.  Callers make the data
 // they publish complete first (s_waitcnt on the loads that filled it).
 __device__ __forceinline__ void barrier_nofence() { __builtin_amdgcn_s_barrier(); }
+
+// s_waitcnt vmcnt(0) that the compiler's wait-count pass sees (unlike an
+// inline-asm wait): after it, registers loaded from global memory count as
+// ready, so no wait for them is placed inside a loop that follows, where it
+// would also wait for the loop's own global -> LDS prefetches.
+__device__ __forceinline__ void wait_vm_known() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // Wait for this wave's outstanding global loads (including global -> LDS).
 __device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
