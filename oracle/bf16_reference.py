@@ -1,6 +1,6 @@
 """bf16 PyTorch reference of the paper's fidelity criterion (test infrastructure).
 
-Sec. 6.6 of the paper accepts forward and gradient errors (against a
+Sec. 6.7 of the paper accepts forward and gradient errors (against a
 high-precision reference) up to twice those of the same attention computed
 with plain bf16 PyTorch operations.  This module is that bf16 computation:
 per sample and per KV group, scores, softmax, output and autograd gradients

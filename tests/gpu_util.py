@@ -53,7 +53,7 @@ def check(name, got, ref, tol=O_TOL, bf16_out=False, ref_bf16=None):
       rounding (half a bf16 ulp of the exact value), which no bf16 result
       can avoid;
     * ``ref_bf16`` (the same attention in plain bf16 PyTorch): the paper's
-      fidelity criterion (Sec. 6.6) -- errors within twice that reference's
+      fidelity criterion (Sec. 6.7) -- errors within twice that reference's
       -- relaxes each bound when the reference itself exceeds half of it.
     """
     got = np.asarray(got, dtype=np.float64)

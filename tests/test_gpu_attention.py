@@ -6,7 +6,7 @@ dQ, dK, dV; max-abs <= 1e-3 for the log-sum-exp.  bf16 outputs meet the
 max-abs bound beyond their own storage rounding (half a bf16 ulp of the exact
 value, which reaches 3e-2 for |dV| >= 8 when many heads and queries are
 summed).  On the small random pools (very short samples, up to 16 query heads
-per KV head) the gradients may instead meet the paper's criterion (Sec. 6.6):
+per KV head) the gradients may instead meet the paper's criterion (Sec. 6.7):
 at most twice the error of the same attention computed in plain bf16
 PyTorch, which itself reaches 2.5e-2 on dK there.
 """

@@ -3,7 +3,7 @@
 * reduced replicas of the pool, 256K-share and 1M-share workloads (same generator, every token count and the
   block size divided by a power of two): every output element against the
   float64 oracle (gradients: the 2e-2 bound, or twice the error of plain bf16
-  PyTorch when that is larger -- the paper's criterion, Sec. 6.6);
+  PyTorch when that is larger -- the paper's criterion, Sec. 6.7);
 * the four large workloads at full size: O, LSE and dQ of sampled query rows (all heads),
   which the oracle computes row by row, and dK / dV from a second backward
   whose dO is zero except on those rows (then only those rows contribute, and
