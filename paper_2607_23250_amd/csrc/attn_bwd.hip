@@ -157,6 +157,7 @@ struct KvShape {
   static constexpr int F_EL = 2 * 2 * kRows;                 // 64 floats as bf16 slots
   static constexpr int STAGE_EL = 2 * Q_EL + F_EL;
   static constexpr int NSTAGE = 8;                            // LDS ring of query blocks
+  static_assert((NSTAGE & (NSTAGE - 1)) == 0, "ring index by mask");
   static constexpr int NQ = kRows * QC / 64 / kWaves;   // wave loads per Q (dO) tile
   static constexpr int LOADS = 2 * NQ;                  // per wave per step (+1 on wave 0)
   static constexpr size_t SMEM = NSTAGE * STAGE_EL * sizeof(bf16);
@@ -183,13 +184,23 @@ __device__ __forceinline__ void wait_stages(int k) {
 }
 
 // Walks the steps (32-row query block x query head) that attend one KV block:
-// tiles in list order, query blocks in row order, heads in order.
+// tiles in list order, query blocks in row order, heads in order.  Per
+// fragment (one tile's rows of the sample) everything a step needs is
+// precomputed, so that advancing is a few 32-bit scalar operations plus two
+// running 64-bit offsets (the Q / dO element offset and the stats offset).
 struct StepIter {
   const libra_tile_t *tiles;
   int64_t T, n_q, n_kv, key0, len;
-  int h_q, g, G, kloc0;
-  int64_t t, fra, frb, qla, m;
-  int h0, h1, h;
+  int h_q, g, G, kloc0, D;
+  int64_t nblk;
+  // fragment
+  int64_t t, row0;          // tile index; buffer row of the fragment's first 32-row block
+  int nm, lo0, hin, qb0;    // blocks; lo of block 0; hi of the last block; q_loc of row0
+  int h0, h1;
+  bool clamp_last;          // the last block runs past the end of the buffer
+  // position
+  int mi, h;
+  int64_t qoff, soff;       // element offset of (row0 + 32 mi, h) in Q / dO; stats offset
   bool valid;
 
   __device__ bool seek() {
@@ -202,27 +213,47 @@ struct StepIter {
       h0 = max(tl.head_begin, g * G);
       h1 = min(tl.head_end, (g + 1) * G);
       if (h0 >= h1) continue;
-      fra = tl.q_row + (pb - tl.q_begin);
-      frb = fra + (pe - pb);
-      qla = pb - key0;
+      const int64_t fra = tl.q_row + (pb - tl.q_begin);
+      const int64_t frb = fra + (pe - pb);
+      const int64_t qla = pb - key0;
       const int64_t first = fra + (kloc0 > qla ? kloc0 - qla : 0);
       if (first >= frb) continue;
-      m = first / kRows;
+      const int64_t mf = first / kRows, ml = (frb - 1) / kRows;
+      row0 = mf * kRows;
+      nm = (int)(ml - mf + 1);
+      lo0 = (int)(fra > row0 ? fra - row0 : 0);
+      hin = (int)(frb - ml * kRows);
+      qb0 = (int)(qla - (fra - row0));
+      clamp_last = ml * kRows + kRows > n_q;
+      mi = 0;
       h = h0;
+      qoff = (row0 * h_q + h0) * D;
+      soff = ((int64_t)h0 * nblk + mf) * 64;
       return true;
     }
     return false;
   }
   __device__ void start() { t = 0; valid = seek(); }
   __device__ void next() {
-    if (++h < h1) return;
+    if (++h < h1) {
+      qoff += D;
+      soff += nblk * 64;
+      return;
+    }
     h = h0;
-    if (++m * kRows < frb) return;
+    if (++mi < nm) {
+      qoff += (int64_t)(kRows * h_q - (h1 - h0 - 1)) * D;
+      soff -= (int64_t)(h1 - h0 - 1) * nblk * 64 - 64;
+      return;
+    }
     ++t;
     valid = seek();
   }
-  __device__ int64_t lo() const { return m * kRows > fra ? m * kRows : fra; }
-  __device__ int64_t hi() const { return (m + 1) * kRows < frb ? (m + 1) * kRows : frb; }
+  __device__ int lo() const { return mi == 0 ? lo0 : 0; }
+  __device__ int hi() const { return mi == nm - 1 ? hin : kRows; }
+  __device__ int qb() const { return qb0 + kRows * mi; }        // q_loc of the block's row 0
+  __device__ bool clamp() const { return clamp_last && mi == nm - 1; }
+  __device__ int64_t m0() const { return row0 + (int64_t)kRows * mi; }
 };
 
 // Instruction order of one dK/dV step (one scheduling region): the S chain
@@ -333,19 +364,18 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
     // fragment are real rows of other fragments or the clamped last row;
     // their P and dS are masked to zero)
     auto issue = [&](const StepIter &st, int sg) {
-      const int64_t m0 = st.m * kRows;
       bf16 *Qs = smem + sg * S::STAGE_EL;
       bf16 *dOs = Qs + S::Q_EL;
       bf16 *Fs = dOs + S::Q_EL;
-      if (m0 + kRows <= n_q) {
-        const size_t qbase = ((size_t)m0 * h_q + st.h) * D;
+      if (!st.clamp()) {
         static_for<S::NQ>([&](auto u) {
           const int wl = w + kWaves * u;
-          g2l16(q + qbase + q_lane[u], Qs + wl * 512);
-          g2l16(dout + qbase + q_lane[u], dOs + wl * 512);
+          g2l16(q + st.qoff + q_lane[u], Qs + wl * 512);
+          g2l16(dout + st.qoff + q_lane[u], dOs + wl * 512);
         });
       } else {
         // the last block of the buffer: rows past it read the last row (masked)
+        const int64_t m0 = st.m0();
         static_for<S::NQ>([&](auto u) {
           const int wl = w + kWaves * u;
           const int r = wl * (64 / S::QC) + l / S::QC;
@@ -355,7 +385,7 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
           g2l16(dout + off, dOs + wl * 512);
         });
       }
-      if (w == 0 && l < 16) g2l16(stats + ((size_t)st.h * nblk + st.m) * 64 + 4 * l, Fs);
+      if (w == 0 && l < 16) g2l16(stats + st.soff + 4 * l, Fs);
     };
 
     // ---- compute one step from the LDS stage at Qs.  Rows of the block are
@@ -455,31 +485,35 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
       });
     };
 
-    StepIter iss{tiles, T, n_q, n_kv, key0, len, h_q, g, G, kloc0};
+    StepIter iss{tiles, T, n_q, n_kv, key0, len, h_q, g, G, kloc0, D, nblk};
     iss.start();
     StepIter cur = iss;
     int issued = 0, computed = 0;
     while (cur.valid) {
       // keep up to NSTAGE - 1 steps in flight, the one computed now included
       while (iss.valid && issued < computed + S::NSTAGE - 1) {
-        issue(iss, issued % S::NSTAGE);
+        issue(iss, issued & (S::NSTAGE - 1));
         iss.next();
         ++issued;
       }
-      const int after = issued - 1 - computed;          // steps issued after this one
-      if (w == 0) wait_stages<S::LOADS + 1, S::NSTAGE - 2>(after);
-      else wait_stages<S::LOADS, S::NSTAGE - 2>(after);
+      // wait for this step's loads: in steady state NSTAGE - 2 later steps
+      // stay in flight; near the end of an item, wait for everything
+      if (issued - 1 - computed >= S::NSTAGE - 2) {
+        if (w == 0) wait_vm_n<(S::NSTAGE - 2) * (S::LOADS + 1)>();
+        else wait_vm_n<(S::NSTAGE - 2) * S::LOADS>();
+      } else {
+        wait_vm_n<0>();
+      }
       barrier_nofence();
 
-      const int64_t m0 = cur.m * kRows;
-      const int lo_l = (int)(cur.lo() - m0), hi_l = (int)(cur.hi() - m0);
-      const int64_t qb = cur.qla + (m0 - cur.fra);            // q_loc of row m0
-      if ((int64_t)kw0 <= qb + hi_l - 1) {
-        const bf16 *Qs = smem + (computed % S::NSTAGE) * S::STAGE_EL;
+      const int lo_l = cur.lo(), hi_l = cur.hi();
+      const int qb = cur.qb();                                  // q_loc of the block's row 0
+      if (kw0 <= qb + hi_l - 1) {
+        const bf16 *Qs = smem + (computed & (S::NSTAGE - 1)) * S::STAGE_EL;
         // interior blocks: every row inside the fragment and at or after every key
         const bool full = lo_l == 0 && hi_l == kRows && wave_keys_ok && kw0 + 31 <= qb;
-        const int64_t need = (int64_t)kl - qb;                // first iq with q_loc >= kl
-        const int lower = (int)(need > lo_l ? (need < kRows ? need : kRows) : lo_l);
+        const int need = kl - qb;                               // first iq with q_loc >= kl
+        const int lower = need > lo_l ? (need < kRows ? need : kRows) : lo_l;
         const int upper = key_ok ? hi_l : 0;
         step(full, Qs, lower, upper);
       }
