@@ -51,6 +51,10 @@ def parse():
                          "1M-cp16-share-qwen3-30b-a3b")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="time budget of the CPU oracle baseline (0 disables it)")
+    ap.add_argument("--vrsp", action="store_true",
+                    help="only measure Variance-Reduced Sequence Placement (Algorithm 1) on the "
+                         "host: time per GBS window and the inter-pool imbalance R - 1 against "
+                         "production-order grouping, on synthetic 256K / 1M windows")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain elementwise copy of a known size (1 GiB read, "
                          "1 GiB written, 3 launches): the reference the HBM byte counters "
@@ -70,6 +74,74 @@ def copy_calibration():
     print(json.dumps({"copy_calibration": {"kernel": "elementwise neg (copy)", "launches": 3,
                                            "read_bytes": 4 * n, "write_bytes": 4 * n}}),
           flush=True)
+
+
+def vrsp_bench(seconds: float):
+    """Algorithm 1 on synthetic optimizer-step windows (one host core)."""
+    import ctypes
+    import paper_2607_23250_amd as pl
+    import workloads as wl
+    from fractions import Fraction
+    L = pl.lib()
+    out_windows = []
+    for kind, gbs in (("256K", 128), ("256K", 256), ("1M", 128), ("1M", 256)):
+        packs = wl.vrsp_window(kind, gbs, seed=1)
+        counts = [len(p) for p in packs]
+        lengths = np.ascontiguousarray(np.concatenate([np.asarray(p, dtype=np.int64)
+                                                       for p in packs]))
+        cu = np.zeros(gbs + 1, dtype=np.int64)
+        cu[1:] = np.cumsum(counts)
+        order = np.zeros(gbs, dtype=np.int64)
+        loads = np.zeros(gbs // 8, dtype=np.int64)
+        args = (pl._ptr(lengths), len(lengths), pl._ptr(cu), gbs, 8, pl._ptr(order),
+                pl._ptr(loads), None)
+        assert L.libra_vrsp(*args) == 0
+        n = 0
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < 0.5:
+            for _ in range(50):
+                L.libra_vrsp(*args)
+            n += 50
+        us = (time.perf_counter() - t0) * 1e6 / n
+        rec = {"window": kind, "gbs": gbs, "pool_size": 8, "samples": int(len(lengths)),
+               "us_per_window": round(us, 2)}
+        if seconds > 0:
+            from oracle import vrsp as ov
+            m = 0
+            t0 = time.perf_counter()
+            while time.perf_counter() - t0 < seconds / 4:
+                ov.vrsp([ov.workload(p) for p in packs], 8)
+                m += 1
+            rec["oracle_us_per_window"] = round((time.perf_counter() - t0) * 1e6 / m, 1)
+        out_windows.append(rec)
+
+    def r_minus_1(loads_, P):
+        return float(Fraction(int(max(loads_)) * len(loads_), int(sum(loads_))) - 1)
+
+    sweep = {}
+    for kind in ("256K", "1M"):
+        rows = {}
+        for P in (1, 2, 4, 8, 16, 32, 64):
+            prod, bal = [], []
+            for seed in range(8):
+                packs = wl.vrsp_window(kind, 128, seed=100 + seed)
+                _, loads, work = pl.libra_vrsp(packs, P)
+                prod.append(r_minus_1(work.reshape(-1, P).sum(axis=1), P))
+                bal.append(r_minus_1(loads, P))
+            rows[str(P)] = {"production_order": round(float(np.mean(prod)), 4),
+                            "vrsp": round(float(np.mean(bal)), 5)}
+        sweep[kind] = rows
+    main = next(r for r in out_windows if r["window"] == "1M" and r["gbs"] == 128)
+    out = {"metric": "VRSP placement time per GBS window (host, one core)",
+           "value": main["us_per_window"], "unit": "us", "higher_is_better": False,
+           "data": "synthetic", "config": {"workload": "1M window, GBS 128, pool size 8"},
+           "windows": out_windows,
+           "imbalance_r_minus_1_gbs128_mean_of_8": sweep}
+    if seconds > 0:
+        out["cpu_baseline"] = {"value": main.get("oracle_us_per_window"), "unit": "us",
+                               "cores": 1, "kind": "oracle",
+                               "sample": "the same 1M window, GBS 128, pool size 8"}
+    print(json.dumps(out), flush=True)
 
 
 def plan(pl, w, q_ranges=None):
@@ -139,6 +211,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.vrsp:
+        vrsp_bench(args.cpu_seconds)
         return
     import torch
     import paper_2607_23250_amd as pl

@@ -113,6 +113,35 @@ int libra_plan(const libra_plan_cfg_t *cfg, const int64_t *lengths, int64_t num_
                int64_t *num_tiles, int64_t *worker_load);
 
 /*
+ * libra_vrsp -- Variance-Reduced Sequence Placement (Sec. 4.2, Algorithm 1;
+ * host only).
+ *
+ * Forms K = num_seqs / pool_size sequence pools of exactly pool_size packed
+ * sequences from one optimizer-step window.  Workload F_i = sum of squared
+ * raw-sample lengths of sequence i (Eq. 4).  Sequences are taken in order
+ * of decreasing F_i, ties by increasing index; each joins the pool of least
+ * (load, pool index) among the pools holding fewer than pool_size
+ * sequences.  The output concatenates the pools in pool-index order
+ * (GA-major, pool-minor), each pool in placement order.
+ *
+ *   lengths[num_samples]: host array, the raw-sample lengths (>= 1) of all
+ *       packed sequences of the window, sequence after sequence.
+ *   seq_cu[num_seqs+1]: host array, sequence i holds samples
+ *       [seq_cu[i], seq_cu[i+1]); seq_cu[0] = 0, seq_cu[num_seqs] =
+ *       num_samples, nondecreasing.
+ *   order[num_seqs]: out, original sequence indices in output order.
+ *   pool_load[num_seqs / pool_size]: out, summed workload of each pool
+ *       (may be NULL).
+ *   seq_work[num_seqs]: out, F_i (may be NULL).
+ * Errors: EINVAL (pool_size < 1 or not dividing num_seqs, inconsistent
+ * offsets or lengths, NULL arguments), EOVERFLOW (a workload or pool load
+ * overflows int64).  Reentrant; allocates only host memory it frees.
+ */
+int libra_vrsp(const int64_t *lengths, int64_t num_samples, const int64_t *seq_cu,
+               int64_t num_seqs, int32_t pool_size, int64_t *order, int64_t *pool_load,
+               int64_t *seq_work);
+
+/*
  * libra_attn_workspace_size -- bytes of device workspace that
  * libra_attn_fwd (backward = 0) or libra_attn_bwd (backward = 1) needs for
  * these sizes.  Returns 0 for invalid sizes.

@@ -31,8 +31,9 @@ TILE_DTYPE = np.dtype([("q_begin", "<i8"), ("q_end", "<i8"), ("q_row", "<i8"), (
                        ("home", "<i4"), ("worker", "<i4"), ("id", "<i4")])
 assert TILE_DTYPE.itemsize == 56
 
-EXPORTED = ("libra_strerror", "libra_last_error", "libra_plan", "libra_attn_workspace_size",
-            "libra_attn_fwd", "libra_attn_bwd", "libra_timing_enable", "libra_timing_read")
+EXPORTED = ("libra_strerror", "libra_last_error", "libra_plan", "libra_vrsp",
+            "libra_attn_workspace_size", "libra_attn_fwd", "libra_attn_bwd",
+            "libra_timing_enable", "libra_timing_read")
 
 
 class LibraError(RuntimeError):
@@ -66,6 +67,8 @@ def lib() -> ctypes.CDLL:
     L.libra_last_error.argtypes = []
     L.libra_plan.restype = ctypes.c_int
     L.libra_plan.argtypes = [ctypes.POINTER(_PlanCfg), P, I64, P, P, P, I32, P, I64, P, P]
+    L.libra_vrsp.restype = ctypes.c_int
+    L.libra_vrsp.argtypes = [P, I64, P, I64, I32, P, P, P]
     L.libra_attn_workspace_size.restype = SZ
     L.libra_attn_workspace_size.argtypes = [I64, I64, I64, I64, I32, I32, I32, I32]
     L.libra_attn_fwd.restype = ctypes.c_int
@@ -129,6 +132,26 @@ def libra_plan(lengths: Sequence[int], pack_tokens: Sequence[int], *, block_toke
     _check(L.libra_plan(*args, _ptr(tiles), len(tiles), ctypes.byref(n_tiles), _ptr(loads)),
            "libra_plan")
     return tiles, loads
+
+
+def libra_vrsp(packs: Sequence[Sequence[int]], pool_size: int
+               ) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Algorithm 1 over one window of packed sequences (each a list of raw
+    sample lengths).  Returns ``(order, pool_load, seq_work)``: original
+    sequence indices in output order, the load of each of the
+    ``len(packs) // pool_size`` pools and every sequence's workload F_i."""
+    L = lib()
+    counts = [len(p) for p in packs]
+    lengths = np.ascontiguousarray(np.concatenate([np.asarray(p, dtype=np.int64) for p in packs])
+                                   if packs else np.zeros(0, dtype=np.int64))
+    seq_cu = _offsets(counts)
+    D = len(packs)
+    order = np.zeros(D, dtype=np.int64)
+    loads = np.zeros(D // pool_size if pool_size > 0 else 0, dtype=np.int64)
+    work = np.zeros(D, dtype=np.int64)
+    _check(L.libra_vrsp(_ptr(lengths), len(lengths), _ptr(seq_cu), D, pool_size, _ptr(order),
+                        _ptr(loads), _ptr(work)), "libra_vrsp")
+    return order, loads, work
 
 
 def libra_attn_workspace_size(num_tiles: int, num_samples: int, n_q_rows: int, n_kv_rows: int,

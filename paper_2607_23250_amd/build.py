@@ -19,7 +19,7 @@ OUT_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "liblibra.so")
 
 HIP_SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "attn_api.hip"]
-CXX_SOURCES = ["plan.cpp"]
+CXX_SOURCES = ["plan.cpp", "vrsp.cpp"]
 ARCH = os.environ.get("LIBRA_OFFLOAD_ARCH", "gfx950")
 
 

@@ -38,6 +38,7 @@ import numpy as np
 __all__ = [
     "LengthLaw", "Workload", "draw_length", "pack_lengths", "workload", "WORKLOADS",
     "W_4K", "W_32K", "W_POOL", "W_256K", "W_1M", "tensors", "tiny_random",
+    "VRSP_WINDOWS", "vrsp_window",
 ]
 
 
@@ -205,6 +206,25 @@ def workload(name: str, scale: int = 1, rank: int = 0) -> Workload:
                         B=8192 // s, H=2, CP=16, q_ranges=_share_ranges(L, 16, rank),
                         notes=["mixture weights 0.95/0.05 assumed"])
     raise AssertionError(name)
+
+
+# Optimizer-step windows of packed sequences (stand-ins for the 256K and 1M
+# production datasets of Sec. 6.1): every pack is filled to exactly its
+# token count from a long-tailed law (median 644, a Pareto tail reaching the
+# pack size), so a few packs carry outliers and most carry many short samples.
+VRSP_WINDOWS = {
+    "256K": (262144, LengthLaw(median=644, sigma=1.5, w_lognormal=0.95, pareto_alpha=1.1,
+                               pareto_xmin=8192, cap=262144)),
+    "1M": (1048576, LengthLaw(median=644, sigma=2.0, w_lognormal=0.95, pareto_alpha=1.05,
+                              pareto_xmin=32768, cap=1048576)),
+}
+
+
+def vrsp_window(kind: str, gbs: int, seed: int) -> List[List[int]]:
+    """``gbs`` packed sequences (lists of raw-sample lengths) of one window."""
+    L, law = VRSP_WINDOWS[kind]
+    rng = np.random.default_rng(50_000 + int(seed))
+    return [pack_lengths(rng, law, L) for _ in range(int(gbs))]
 
 
 def tensors(seed: int, n_q: int, n_k: int, h_q: int, h_kv: int, d: int,
