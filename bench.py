@@ -55,6 +55,10 @@ def parse():
                     help="only measure Variance-Reduced Sequence Placement (Algorithm 1) on the "
                          "host: time per GBS window and the inter-pool imbalance R - 1 against "
                          "production-order grouping, on synthetic 256K / 1M windows")
+    ap.add_argument("--straggler", action="store_true",
+                    help="one-GPU straggler emulation on the 1M-token pack: fwd+bwd time of each "
+                         "of the 16 zigzag CP rank shares vs each of the 16 Libra worker tile "
+                         "sets (Algorithm 2), plus throughput per call vs block length x heads")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain elementwise copy of a known size (1 GiB read, "
                          "1 GiB written, 3 launches): the reference the HBM byte counters "
@@ -144,6 +148,111 @@ def vrsp_bench(seconds: float):
     print(json.dumps(out), flush=True)
 
 
+def straggler_bench():
+    """Zigzag CP (every rank computes its head+tail share) against Libra's
+    worker tile sets of the same 1,048,576-token pack, one set at a time on
+    one GPU; the slowest set stands for the step's straggler.  Then the
+    throughput of single calls of one tile (B rows x heads) from the middle
+    of the 900K sample."""
+    import torch
+    import paper_2607_23250_amd as pl
+    import workloads as wl
+    dev = torch.device("cuda:0")
+    w0 = wl.workload(wl.W_1M)
+    cp = w0.CP
+    g = torch.Generator(device=dev).manual_seed(11)
+
+    def rnd(shape):
+        return torch.randn(shape, device=dev, generator=g, dtype=torch.float32).to(torch.bfloat16)
+
+    n_all = w0.n_kv_rows
+    k = rnd((n_all, w0.h_kv, w0.d))
+    v = rnd((n_all, w0.h_kv, w0.d))
+    cu = np.zeros(len(w0.lengths) + 1, dtype=np.int64)
+    cu[1:] = np.cumsum(w0.lengths)
+    cud = torch.from_numpy(cu).to(dev)
+    dk = torch.zeros((n_all, w0.h_kv, w0.d), dtype=torch.float32, device=dev)
+    dv = torch.zeros_like(dk)
+
+    def run_set(tiles, n_rows, q, do, o, lse, dq, reps=2):
+        td = pl.tiles_to_device(tiles, dev)
+        ws = pl.alloc_workspace(max(pl.libra_attn_workspace_size(len(tiles), len(w0.lengths),
+                                                                   n_rows, n_all, w0.h_q,
+                                                                   w0.h_kv, w0.d, b)
+                                    for b in (False, True)), dev)
+        times = []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            pl.libra_attn_fwd(q, k, v, cud, td, o=o, lse=lse, workspace=ws)
+            pl.libra_attn_bwd(q, k, v, o, lse, do, cud, td, dq=dq, dk=dk, dv=dv,
+                              accumulate=True, workspace=ws)
+            torch.cuda.synchronize()
+            times.append(time.perf_counter() - t0)
+        return min(times) * 1e3
+
+    def flops(tiles):
+        return 14.0 * w0.d * float(tiles["cost"].sum())
+
+    # zigzag CP: rank r computes its head + tail chunk against every causal key
+    share_rows = w0.n_q_rows
+    q = rnd((share_rows, w0.h_q, w0.d))
+    do = rnd((share_rows, w0.h_q, w0.d))
+    o = torch.empty_like(q)
+    dq = torch.empty_like(q)
+    lse = torch.empty((w0.h_q, share_rows), dtype=torch.float32, device=dev)
+    zig = []
+    for r in range(cp):
+        wr = wl.workload(wl.W_1M, rank=r)
+        tiles = plan(pl, wr, wr.q_ranges)[0]
+        ms = run_set(tiles, share_rows, q, do, o, lse, dq)
+        zig.append({"rank": r, "ms": round(ms, 2), "tflop": round(flops(tiles) / 1e12, 2)})
+        print(json.dumps({"zigzag_rank": zig[-1]}), file=sys.stderr, flush=True)
+    del q, do, o, dq, lse
+    # Libra: the whole pack planned over the same 16 workers
+    full, loads = plan(pl, w0)
+    q = rnd((n_all, w0.h_q, w0.d))
+    do = rnd((n_all, w0.h_q, w0.d))
+    o = torch.empty_like(q)
+    dq = torch.empty_like(q)
+    lse = torch.empty((w0.h_q, n_all), dtype=torch.float32, device=dev)
+    lib = []
+    for r in range(cp):
+        tiles = full[full["worker"] == r]
+        ms = run_set(tiles, n_all, q, do, o, lse, dq)
+        lib.append({"worker": r, "ms": round(ms, 2), "tflop": round(flops(tiles) / 1e12, 2)})
+        print(json.dumps({"libra_worker": lib[-1]}), file=sys.stderr, flush=True)
+    # throughput per call: one tile of B rows x heads ending at row 450K of the
+    # 900K sample (the pack's last sample)
+    j = len(w0.lengths) - 1
+    heat = {}
+    for B in (1024, 2048, 4096, 8192, 16384):
+        for heads in (2, 4, 8, 16, 32):
+            end = int(cu[j]) + 450000
+            t = np.zeros(1, dtype=pl.TILE_DTYPE)
+            t["q_begin"], t["q_end"], t["q_row"] = end - B, end, end - B
+            loc = np.arange(end - B, end) - cu[j]
+            t["cost"] = heads * int((loc + 1).sum())
+            t["head_begin"], t["head_end"] = 0, heads
+            ms = run_set(t, n_all, q, do, o, lse, dq, reps=3)
+            heat[f"B{B}_h{heads}"] = round(flops(t) / (ms * 1e-3) / 1e12, 1)
+    zmax = max(x["ms"] for x in zig)
+    lmax = max(x["ms"] for x in lib)
+    out = {"metric": "one-GPU straggler emulation, 1M-token pack, 16 workers (fwd+bwd)",
+           "value": round(zmax / lmax, 3), "unit": "x (zigzag max / Libra max)",
+           "higher_is_better": True, "data": "synthetic",
+           "config": {"workload": "1M-token pack (packs of the 1M workload), CP=16, B=8192, H=2"},
+           "zigzag": {"max_ms": zmax, "mean_ms": round(float(np.mean([x["ms"] for x in zig])), 2),
+                      "max_over_mean": round(zmax / float(np.mean([x["ms"] for x in zig])), 4),
+                      "ranks": zig},
+           "libra": {"max_ms": lmax, "mean_ms": round(float(np.mean([x["ms"] for x in lib])), 2),
+                     "max_over_mean": round(lmax / float(np.mean([x["ms"] for x in lib])), 4),
+                     "plan_load_max_over_mean": round(float(cp * loads.max() / loads.sum()), 4),
+                     "workers": lib},
+           "tflops_per_call_tile_B_x_heads": heat}
+    print(json.dumps(out), flush=True)
+
+
 def plan(pl, w, q_ranges=None):
     return pl.libra_plan(w.lengths, w.pack_tokens, block_tokens=w.B, head_shards=w.H, cp=w.CP,
                          num_q_heads=w.h_q, num_kv_heads=w.h_kv, head_dim=w.d, q_ranges=q_ranges)
@@ -206,14 +315,17 @@ def cpu_baseline(w, q, k, v, do, seconds):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
-              "(the multi-GPU exchange of the paper is out of scope here)", file=sys.stderr)
+        print(f"bench.py runs on one GPU; --gpus {args.gpus} is not supported (the "
+              "multi-GPU tile exchange of the paper is not implemented)", file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
         return
     if args.vrsp:
         vrsp_bench(args.cpu_seconds)
+        return
+    if args.straggler:
+        straggler_bench()
         return
     import torch
     import paper_2607_23250_amd as pl
