@@ -103,6 +103,10 @@ const char *libra_last_error(void);
  *   tiles[tiles_cap]: output in tile-ID order, or NULL to query the count.
  *   num_tiles: out, number of tiles (also set when tiles is NULL).
  *   worker_load[V]: out, Algorithm 2 load L_r of every worker (may be NULL).
+ *   worker_bytes[V]: out, bytes every worker receives under the plan (may be
+ *       NULL): the sum of Eq. 8 over the tiles placed on it, each evaluated
+ *       when the tile was placed (KV groups not yet held, plus Q rows and
+ *       outputs of tiles it does not home).
  * Errors: EINVAL (inconsistent inputs), ENOSPC (tiles_cap too small;
  * *num_tiles still holds the count), EOVERFLOW (a cost or byte count
  * overflows int64).  Reentrant; allocates only host memory it frees.
@@ -110,7 +114,7 @@ const char *libra_last_error(void);
 int libra_plan(const libra_plan_cfg_t *cfg, const int64_t *lengths, int64_t num_samples,
                const int64_t *cu_seqlens, const int64_t *pack_cu, const int64_t *q_ranges,
                int32_t num_q_ranges, libra_tile_t *tiles, int64_t tiles_cap,
-               int64_t *num_tiles, int64_t *worker_load);
+               int64_t *num_tiles, int64_t *worker_load, int64_t *worker_bytes);
 
 /*
  * libra_vrsp -- Variance-Reduced Sequence Placement (Sec. 4.2, Algorithm 1;

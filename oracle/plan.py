@@ -72,6 +72,7 @@ class Tile:
     home: int
     worker: int = -1
     samples: Tuple[int, ...] = ()     # sample indices j of K(t)
+    comm: int = 0                     # Delta_comm(t, worker) when it was placed (Eq. 8)
 
 
 def sample_offsets(lengths: Sequence[int]) -> List[int]:
@@ -194,6 +195,7 @@ def place(cfg: PlanCfg, tiles: List[Tile], lengths: Sequence[int],
         else:
             r_star = min(range(V), key=lambda r: (L[r], dc[r], r))
         t.worker = r_star
+        t.comm = dc[r_star]
         L[r_star] += t.cost
         h = t.id % cfg.H
         for j in t.samples:
@@ -207,6 +209,17 @@ def plan(cfg: PlanCfg, lengths: Sequence[int], pack_tokens: Sequence[int],
     tiles = build_tiles(cfg, lengths, pack_tokens, q_ranges)
     loads = place(cfg, tiles, lengths, pack_tokens)
     return tiles, loads
+
+
+def worker_comm(tiles: Sequence[Tile], V: int) -> List[int]:
+    """Bytes each worker receives under the plan: the sum of Eq. 8 over the
+    tiles placed on it, each taken when the tile was placed (KV groups it
+    did not hold yet, plus the tile's Q rows and outputs when it is not the
+    tile's Q-home)."""
+    B = [0] * V
+    for t in tiles:
+        B[t.worker] += t.comm
+    return B
 
 
 def max_over_mean(loads: Sequence[int]) -> float:

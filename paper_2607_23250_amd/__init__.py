@@ -66,7 +66,7 @@ def lib() -> ctypes.CDLL:
     L.libra_last_error.restype = ctypes.c_char_p
     L.libra_last_error.argtypes = []
     L.libra_plan.restype = ctypes.c_int
-    L.libra_plan.argtypes = [ctypes.POINTER(_PlanCfg), P, I64, P, P, P, I32, P, I64, P, P]
+    L.libra_plan.argtypes = [ctypes.POINTER(_PlanCfg), P, I64, P, P, P, I32, P, I64, P, P, P]
     L.libra_vrsp.restype = ctypes.c_int
     L.libra_vrsp.argtypes = [P, I64, P, I64, I32, P, P, P]
     L.libra_attn_workspace_size.restype = SZ
@@ -106,12 +106,13 @@ def _offsets(counts) -> np.ndarray:
 def libra_plan(lengths: Sequence[int], pack_tokens: Sequence[int], *, block_tokens: int,
                head_shards: int, cp: int, num_q_heads: int, num_kv_heads: int, head_dim: int,
                elem_bytes: int = 2, tau: Tuple[int, int] = (3, 100),
-               q_ranges: Optional[Sequence[Tuple[int, int]]] = None
-               ) -> Tuple[np.ndarray, np.ndarray]:
+               q_ranges: Optional[Sequence[Tuple[int, int]]] = None, with_bytes: bool = False
+               ):
     """SH-Tiles with Eq. 6 costs and the Algorithm 2 placement.
 
     Returns ``(tiles, loads)``: a ``TILE_DTYPE`` array in tile-ID order and the
-    int64 load of each of the ``len(pack_tokens) * cp`` workers.
+    int64 load of each of the ``len(pack_tokens) * cp`` workers; with
+    ``with_bytes``, also the bytes each worker receives under the plan.
     """
     L = lib()
     lengths = np.ascontiguousarray(lengths, dtype=np.int64)
@@ -126,12 +127,13 @@ def libra_plan(lengths: Sequence[int], pack_tokens: Sequence[int], *, block_toke
         nqr = len(qr) // 2
     n_tiles = ctypes.c_int64(0)
     args = (ctypes.byref(cfg), _ptr(lengths), len(lengths), _ptr(cu), _ptr(pack_cu), _ptr(qr), nqr)
-    _check(L.libra_plan(*args, None, 0, ctypes.byref(n_tiles), None), "libra_plan")
+    _check(L.libra_plan(*args, None, 0, ctypes.byref(n_tiles), None, None), "libra_plan")
     tiles = np.zeros(n_tiles.value, dtype=TILE_DTYPE)
     loads = np.zeros(len(pack_tokens) * cp, dtype=np.int64)
-    _check(L.libra_plan(*args, _ptr(tiles), len(tiles), ctypes.byref(n_tiles), _ptr(loads)),
-           "libra_plan")
-    return tiles, loads
+    recv = np.zeros(len(pack_tokens) * cp, dtype=np.int64) if with_bytes else None
+    _check(L.libra_plan(*args, _ptr(tiles), len(tiles), ctypes.byref(n_tiles), _ptr(loads),
+                        _ptr(recv)), "libra_plan")
+    return (tiles, loads, recv) if with_bytes else (tiles, loads)
 
 
 def libra_vrsp(packs: Sequence[Sequence[int]], pool_size: int

@@ -102,7 +102,8 @@ extern "C" const char *libra_last_error(void) { return last_error_text().c_str()
 extern "C" int libra_plan(const libra_plan_cfg_t *cfg, const int64_t *lengths,
                           int64_t num_samples, const int64_t *cu, const int64_t *pack_cu,
                           const int64_t *q_ranges, int32_t num_q_ranges, libra_tile_t *out,
-                          int64_t tiles_cap, int64_t *num_tiles, int64_t *worker_load) {
+                          int64_t tiles_cap, int64_t *num_tiles, int64_t *worker_load,
+                          int64_t *worker_bytes) {
   last_error_text().clear();
   if (int rc = validate(cfg, lengths, num_samples, cu, pack_cu)) return rc;
   if (!num_tiles) return fail(LIBRA_EINVAL, "num_tiles is NULL");
@@ -207,7 +208,7 @@ extern "C" int libra_plan(const libra_plan_cfg_t *cfg, const int64_t *lengths,
     if (tiles[a].cost != tiles[b].cost) return tiles[a].cost > tiles[b].cost;
     return tiles[a].id < tiles[b].id;
   });
-  std::vector<i64> load(V, 0);
+  std::vector<i64> load(V, 0), received(V, 0);
   std::vector<int32_t> assign(T, -1);
   std::vector<i64> delta(V);
   for (i64 idx : order) {
@@ -236,7 +237,10 @@ extern "C" int libra_plan(const libra_plan_cfg_t *cfg, const int64_t *lengths,
     }
     assign[idx] = (int32_t)best;
     if (!fits_i64((i128)load[best] + t.cost)) return fail(LIBRA_EOVERFLOW, "load overflows");
+    if (!fits_i64((i128)received[best] + delta[best]))
+      return fail(LIBRA_EOVERFLOW, "received bytes overflow int64");
     load[best] += t.cost;
+    received[best] += delta[best];
     for (i64 s = t.s_first; s <= t.s_last; ++s)
       resident[(size_t)((s * H + t.shard) * V + best)] = 1;
   }
@@ -258,5 +262,6 @@ extern "C" int libra_plan(const libra_plan_cfg_t *cfg, const int64_t *lengths,
     }
   }
   if (worker_load) std::memcpy(worker_load, load.data(), sizeof(i64) * V);
+  if (worker_bytes) std::memcpy(worker_bytes, received.data(), sizeof(i64) * V);
   return LIBRA_OK;
 }

@@ -4,7 +4,8 @@
 * total cost against the closed form h_q * sum_j l_j (l_j + 1) / 2 (Eq. 2 up to
   the causal constant), and a single-sample closed form per block;
 * the Sec. 1 example (one 40K sample is about 10x ten 4K samples);
-* Algorithm 2 on hand-worked examples (tests/golden), its load bound, full
+* Algorithm 2 on hand-worked examples (tests/golden: placement, loads and
+  the bytes each worker receives), its load bound, full
   coverage, and a comparison with exhaustive search on tiny inputs.
 """
 import itertools
@@ -86,6 +87,7 @@ def test_worked_examples():
                 "home": t.home, "worker": t.worker} for t in tiles]
         assert got == ex["tiles"], ex["name"]
         assert loads == ex["loads"], ex["name"]
+        assert op.worker_comm(tiles, cfg.V) == ex["received"], ex["name"]
 
 
 def test_zigzag_home_layout():

@@ -1,6 +1,6 @@
 """libra_plan (C++) against the plan oracle: bit-exact tiles, costs,
-placement and loads on the five workloads and on random small inputs; error
-paths forced from the host."""
+placement, loads and received bytes on the five workloads and on random
+small inputs; error paths forced from the host."""
 import numpy as np
 import pytest
 
@@ -13,18 +13,19 @@ def _native(w, q_ranges=None, **over):
     kw = dict(block_tokens=w.B, head_shards=w.H, cp=w.CP, num_q_heads=w.h_q,
               num_kv_heads=w.h_kv, head_dim=w.d)
     kw.update(over)
-    return pl.libra_plan(w.lengths, w.pack_tokens, q_ranges=q_ranges, **kw)
+    return pl.libra_plan(w.lengths, w.pack_tokens, q_ranges=q_ranges, with_bytes=True, **kw)
 
 
 def _oracle(w, q_ranges=None, elem_bytes=2, tau=(3, 100)):
     cfg = op.PlanCfg(B=w.B, H=w.H, P=w.P, CP=w.CP, h_q=w.h_q, h_kv=w.h_kv, d=w.d,
                      elem_bytes=elem_bytes, tau_num=tau[0], tau_den=tau[1])
-    return op.plan(cfg, w.lengths, w.pack_tokens, q_ranges)
+    tiles, loads = op.plan(cfg, w.lengths, w.pack_tokens, q_ranges)
+    return tiles, loads, op.worker_comm(tiles, cfg.V)
 
 
 def _same(native, oracle):
-    tiles, loads = native
-    otiles, oloads = oracle
+    tiles, loads, recv = native
+    otiles, oloads, orecv = oracle
     assert len(tiles) == len(otiles)
     for a, b in zip(tiles, otiles):
         got = (int(a["id"]), int(a["pack"]), int(a["q_begin"]), int(a["q_end"]), int(a["q_row"]),
@@ -34,6 +35,7 @@ def _same(native, oracle):
                 b.home, b.worker)
         assert got == want
     assert [int(x) for x in loads] == list(oloads)
+    assert [int(x) for x in recv] == list(orecv)
 
 
 @pytest.mark.parametrize("name", wl.WORKLOADS)
@@ -47,7 +49,7 @@ def test_workloads_bit_exact(name):
 @pytest.mark.parametrize("name", wl.WORKLOADS)
 def test_workloads_meet_load_target(name):
     w = wl.workload(name)
-    tiles, loads = _native(w)
+    tiles, loads, _ = _native(w)
     assert w.V * loads.max() / loads.sum() <= 1.05
 
 
@@ -83,7 +85,7 @@ def test_random_q_ranges_bit_exact(seed):
 
 def test_size_query_and_enospc():
     w = wl.workload(wl.W_32K)
-    tiles, _ = _native(w)
+    tiles, _, _ = _native(w)
     import ctypes
     L = pl.lib()
     lengths = np.asarray(w.lengths, dtype=np.int64)
@@ -93,7 +95,7 @@ def test_size_query_and_enospc():
     n = ctypes.c_int64(-1)
     out = np.zeros(3, dtype=pl.TILE_DTYPE)
     rc = L.libra_plan(ctypes.byref(cfg), pl._ptr(lengths), len(lengths), pl._ptr(cu), pl._ptr(pcu),
-                      None, 0, pl._ptr(out), 3, ctypes.byref(n), None)
+                      None, 0, pl._ptr(out), 3, ctypes.byref(n), None, None)
     assert rc == pl.LIBRA_ENOSPC and n.value == len(tiles)
 
 
