@@ -59,6 +59,10 @@ def parse():
                     help="one-GPU straggler emulation on the 1M-token pack: fwd+bwd time of each "
                          "of the 16 zigzag CP rank shares vs each of the 16 Libra worker tile "
                          "sets (Algorithm 2), plus throughput per call vs block length x heads")
+    ap.add_argument("--simulate", action="store_true",
+                    help="offline planner simulation (host only): the LLN estimate of Eq. 3 "
+                         "against production-order grouping, and TAP's (B, H) grid on "
+                         "VRSP-formed pools: load balance and exchanged bytes per worker")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain elementwise copy of a known size (1 GiB read, "
                          "1 GiB written, 3 launches): the reference the HBM byte counters "
@@ -253,6 +257,62 @@ def straggler_bench():
     print(json.dumps(out), flush=True)
 
 
+def simulate():
+    """Planner-only simulation on synthetic optimizer-step windows."""
+    import math
+    import paper_2607_23250_amd as pl
+    import workloads as wl
+    out = {"metric": "offline (P, H, B) simulation of the planner (host only)",
+           "data": "synthetic", "lln": {}, "grid": {}}
+    # (1) Eq. 3: E[R] ~ 1 + CV / sqrt(P) * sqrt(2 ln(D / P)) for random grouping
+    for kind in ("256K", "1M"):
+        rows = {}
+        wins = [wl.vrsp_window(kind, 128, seed=200 + s) for s in range(8)]
+        for P in (1, 2, 4, 8, 16, 32, 64):
+            meas, pred = [], []
+            for packs in wins:
+                _, _, F = pl.libra_vrsp(packs, P)
+                Ff = F.astype(np.float64)
+                loads = Ff.reshape(-1, P).sum(axis=1)
+                meas.append(loads.max() / (P * Ff.mean()))
+                cv = Ff.std() / Ff.mean()
+                pred.append(1 + cv / math.sqrt(P) * math.sqrt(2 * math.log(len(F) / P)))
+            rows[str(P)] = {"measured_R": round(float(np.mean(meas)), 3),
+                            "eq3_R": round(float(np.mean(pred)), 3)}
+        out["lln"][kind] = rows
+    # (2) TAP grid on VRSP pools (Sec. 6.6 settings)
+    grids = {"256K": dict(cp=8, P=8, gbs=128, h_q=32, h_kv=16, Bs=(2048, 4096, 8192, 16384)),
+             "1M": dict(cp=16, P=4, gbs=32, h_q=32, h_kv=4, Bs=(4096, 8192, 16384, 32768))}
+    for kind, g in grids.items():
+        packs = wl.vrsp_window(kind, g["gbs"], seed=300)
+        order, _, _ = pl.libra_vrsp(packs, g["P"])
+        pools = [[packs[i] for i in order[k * g["P"]:(k + 1) * g["P"]]]
+                 for k in range(g["gbs"] // g["P"])]
+        res = {}
+        for B in g["Bs"]:
+            for H in (1, 2, 4, 8):
+                mm, recv_max, recv_tot, ms = [], [], [], []
+                for pool in pools:
+                    lengths = [x for pk in pool for x in pk]
+                    t0 = time.perf_counter()
+                    tiles, loads, recv = pl.libra_plan(
+                        lengths, [sum(pk) for pk in pool], block_tokens=B, head_shards=H,
+                        cp=g["cp"], num_q_heads=g["h_q"], num_kv_heads=g["h_kv"], head_dim=128,
+                        with_bytes=True)
+                    ms.append((time.perf_counter() - t0) * 1e3)
+                    mm.append(len(loads) * loads.max() / loads.sum())
+                    recv_max.append(recv.max())
+                    recv_tot.append(recv.sum())
+                res[f"B{B}_H{H}"] = {
+                    "tiles_per_pack": int(len(tiles) // g["P"]),
+                    "max_over_mean_load": round(float(np.mean(mm)), 4),
+                    "max_worker_recv_GB": round(float(np.mean(recv_max)) / 1e9, 3),
+                    "pool_recv_GB": round(float(np.mean(recv_tot)) / 1e9, 2),
+                    "plan_ms": round(float(np.mean(ms)), 2)}
+        out["grid"][kind] = {"setting": {k: v for k, v in g.items() if k != "Bs"}, "cells": res}
+    print(json.dumps(out), flush=True)
+
+
 def plan(pl, w, q_ranges=None):
     return pl.libra_plan(w.lengths, w.pack_tokens, block_tokens=w.B, head_shards=w.H, cp=w.CP,
                          num_q_heads=w.h_q, num_kv_heads=w.h_kv, head_dim=w.d, q_ranges=q_ranges)
@@ -326,6 +386,9 @@ def main():
         return
     if args.straggler:
         straggler_bench()
+        return
+    if args.simulate:
+        simulate()
         return
     import torch
     import paper_2607_23250_amd as pl
