@@ -155,11 +155,12 @@ struct KvShape {
   static constexpr int QC = D / 8;          // 16-byte columns of a Q / dO row
   static constexpr int Q_EL = kRows * D;
   static constexpr int F_EL = 2 * 2 * kRows;                 // 64 floats as bf16 slots
-  static constexpr int STAGE_EL = 2 * Q_EL + F_EL;
-  static constexpr int NSTAGE = 8;                            // LDS ring of query blocks
+  static constexpr int HEAD_EL = 2 * Q_EL + F_EL;             // Q, dO, stats of one head
+  static constexpr int STAGE_EL = 2 * HEAD_EL;                // a step is two query heads
+  static constexpr int NSTAGE = 4;                            // LDS ring of steps
   static_assert((NSTAGE & (NSTAGE - 1)) == 0, "ring index by mask");
   static constexpr int NQ = kRows * QC / 64 / kWaves;   // wave loads per Q (dO) tile
-  static constexpr int LOADS = 2 * NQ;                  // per wave per step (+1 on wave 0)
+  static constexpr int LOADS = 4 * NQ;                  // per wave per step (+1 on waves 0, 1)
   static constexpr size_t SMEM = NSTAGE * STAGE_EL * sizeof(bf16);
   static_assert((NSTAGE - 2) * (LOADS + 1) <= 63, "vmcnt range");
 };
@@ -234,21 +235,25 @@ struct StepIter {
     return false;
   }
   __device__ void start() { t = 0; valid = seek(); }
+  // steps are pairs of query heads (h, h + 1); two() is false for the last
+  // step of an odd head count
   __device__ void next() {
-    if (++h < h1) {
-      qoff += D;
-      soff += nblk * 64;
+    if ((h += 2) < h1) {
+      qoff += 2 * D;
+      soff += 2 * nblk * 64;
       return;
     }
+    const int back = h - 2 - h0;                 // heads advanced within this block
     h = h0;
     if (++mi < nm) {
-      qoff += (int64_t)(kRows * h_q - (h1 - h0 - 1)) * D;
-      soff -= (int64_t)(h1 - h0 - 1) * nblk * 64 - 64;
+      qoff += (int64_t)(kRows * h_q - back) * D;
+      soff -= (int64_t)back * nblk * 64 - 64;
       return;
     }
     ++t;
     valid = seek();
   }
+  __device__ bool two() const { return h + 1 < h1; }
   __device__ int lo() const { return mi == 0 ? lo0 : 0; }
   __device__ int hi() const { return mi == nm - 1 ? hin : kRows; }
   __device__ int qb() const { return qb0 + kRows * mi; }        // q_loc of the block's row 0
@@ -364,28 +369,35 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
     // fragment are real rows of other fragments or the clamped last row;
     // their P and dS are masked to zero)
     auto issue = [&](const StepIter &st, int sg) {
-      bf16 *Qs = smem + sg * S::STAGE_EL;
-      bf16 *dOs = Qs + S::Q_EL;
-      bf16 *Fs = dOs + S::Q_EL;
-      if (!st.clamp()) {
-        static_for<S::NQ>([&](auto u) {
-          const int wl = w + kWaves * u;
-          g2l16(q + st.qoff + q_lane[u], Qs + wl * 512);
-          g2l16(dout + st.qoff + q_lane[u], dOs + wl * 512);
-        });
-      } else {
-        // the last block of the buffer: rows past it read the last row (masked)
-        const int64_t m0 = st.m0();
-        static_for<S::NQ>([&](auto u) {
-          const int wl = w + kWaves * u;
-          const int r = wl * (64 / S::QC) + l / S::QC;
-          const int64_t row = m0 + r < n_q ? m0 + r : n_q - 1;
-          const size_t off = ((size_t)row * h_q + st.h) * D + 8 * swt<S::QC>(r, l % S::QC);
-          g2l16(q + off, Qs + wl * 512);
-          g2l16(dout + off, dOs + wl * 512);
-        });
-      }
-      if (w == 0 && l < 16) g2l16(stats + st.soff + 4 * l, Fs);
+      // head h into the first half of the stage, head h + 1 (or h again when
+      // the step has one head; it is then not computed) into the second
+      const int64_t dq2 = st.two() ? D : 0, ds2 = st.two() ? nblk * 64 : 0;
+      static_for<2>([&](auto hb) {
+        bf16 *Qs = smem + sg * S::STAGE_EL + hb * S::HEAD_EL;
+        bf16 *dOs = Qs + S::Q_EL;
+        bf16 *Fs = dOs + S::Q_EL;
+        const int64_t qo = st.qoff + (hb ? dq2 : 0);
+        if (!st.clamp()) {
+          static_for<S::NQ>([&](auto u) {
+            const int wl = w + kWaves * u;
+            g2l16(q + qo + q_lane[u], Qs + wl * 512);
+            g2l16(dout + qo + q_lane[u], dOs + wl * 512);
+          });
+        } else {
+          // the last block of the buffer: rows past it read the last row (masked)
+          const int64_t m0 = st.m0();
+          const int hh = st.h + (hb && st.two() ? 1 : 0);
+          static_for<S::NQ>([&](auto u) {
+            const int wl = w + kWaves * u;
+            const int r = wl * (64 / S::QC) + l / S::QC;
+            const int64_t row = m0 + r < n_q ? m0 + r : n_q - 1;
+            const size_t off = ((size_t)row * h_q + hh) * D + 8 * swt<S::QC>(r, l % S::QC);
+            g2l16(q + off, Qs + wl * 512);
+            g2l16(dout + off, dOs + wl * 512);
+          });
+        }
+        if (w == hb && l < 16) g2l16(stats + st.soff + (hb ? ds2 : 0) + 4 * l, Fs);
+      });
     };
 
     // ---- compute one step from the LDS stage at Qs.  Rows of the block are
@@ -499,7 +511,7 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
       // wait for this step's loads: in steady state NSTAGE - 2 later steps
       // stay in flight; near the end of an item, wait for everything
       if (issued - 1 - computed >= S::NSTAGE - 2) {
-        if (w == 0) wait_vm_n<(S::NSTAGE - 2) * (S::LOADS + 1)>();
+        if (w < 2) wait_vm_n<(S::NSTAGE - 2) * (S::LOADS + 1)>();
         else wait_vm_n<(S::NSTAGE - 2) * S::LOADS>();
       } else {
         wait_vm_n<0>();
@@ -510,12 +522,14 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
       const int qb = cur.qb();                                  // q_loc of the block's row 0
       if (kw0 <= qb + hi_l - 1) {
         const bf16 *Qs = smem + (computed & (S::NSTAGE - 1)) * S::STAGE_EL;
+        const bool two = cur.two();
         // interior blocks: every row inside the fragment and at or after every key
         const bool full = lo_l == 0 && hi_l == kRows && wave_keys_ok && kw0 + 31 <= qb;
         const int need = kl - qb;                               // first iq with q_loc >= kl
         const int lower = need > lo_l ? (need < kRows ? need : kRows) : lo_l;
         const int upper = key_ok ? hi_l : 0;
         step(full, Qs, lower, upper);
+        if (two) step(full, Qs + S::HEAD_EL, lower, upper);
       }
       ++computed;
       cur.next();
