@@ -261,34 +261,6 @@ struct StepIter {
   __device__ int64_t m0() const { return row0 + (int64_t)kRows * mi; }
 };
 
-// Instruction order of one dK/dV step (one scheduling region): the S chain
-// with the Q / dO row reads, then the dP chain with the P = exp(...) VALU
-// work and the transpose reads of dO, then dV^T with the dS VALU work and the
-// transpose reads of Q, then dK^T.  With one wave per SIMD only this
-// interleaving overlaps VALU and LDS latency with the matrix cores.
-template <int NC, int NT, int VA, int VB>
-__device__ __forceinline__ void sched_kv_step() {
-  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-#pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-  }
-#pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x002, VA, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-  }
-#pragma unroll
-  for (int i = 0; i < NT; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x002, VB, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-  }
-  __builtin_amdgcn_sched_group_barrier(0x008, NT, 0);
-}
-
 template <int D>
 __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) void attn_bwd_dkdv_kernel(
     const bf16 *__restrict__ k, const bf16 *__restrict__ v, const bf16 *__restrict__ q,

@@ -137,16 +137,6 @@ struct BwdItem {
   int32_t pad;
 };
 
-// Offset of sample j in the padded, transposed V copy: sample j starts at a
-// multiple of kFwdBN and owns ceil(len/kFwdBN)*kFwdBN zero-padded slots.
-// ceil64(cu[j] + 128 j) keeps consecutive samples apart without a prefix sum.
-__host__ __device__ inline int64_t vt_offset(int64_t cu_j, int64_t j) {
-  return (cu_j + 128 * j + 63) / 64 * 64;
-}
-__host__ __device__ inline int64_t vt_pitch(int64_t n_kv, int64_t n_samples) {
-  return n_kv + 128 * n_samples + 64;
-}
-
 // Swap bits 2 and 3 of a row index: reading MFMA operand rows in this order
 // makes the 16 accumulator registers of a lane hold 8 + 8 contiguous rows.
 __device__ __forceinline__ int perm32(int m) {
@@ -157,36 +147,7 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-// acc += A B with the accumulator pinned to AGPRs (inline asm: the compiler's
-// MFMA form is chosen per function, and kernels whose long-lived
-// accumulators must not occupy the 256 architectural VGPRs use this one).
-// The two leading wait states cover a VALU write of A or B or of the
-// accumulator (zero-initialisation) immediately before.  Reading acc with
-// VALU or memory instructions afterwards needs mfma_acc_drain first.
-__device__ __forceinline__ void mfma32_agpr(f32x16 &acc, bf16x8 a, bf16x8 b) {
-  asm("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
-}
-// acc = 0 in AGPRs (an MFMA of zero operands with a zero accumulator), so that
-// the accumulator never lives in VGPRs.
-__device__ __forceinline__ void mfma_agpr_zero(f32x16 &acc) {
-  const bf16x8 z = {};
-  asm("v_mfma_f32_32x32x16_bf16 %0, %1, %1, 0" : "=a"(acc) : "v"(z));
-}
-// Wait states between the last mfma32_agpr into acc and any other read of it.
-__device__ __forceinline__ void mfma_acc_drain(f32x16 &a0, f32x16 &a1) {
-  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3" : "+a"(a0), "+a"(a1));
-}
-
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-
-// LDS tiles are stored without padding; the 16-byte column of a row is
-// XOR-swizzled with the row index so that the 16 lanes that read 16
-// consecutive rows at the same logical column hit 16 different bank groups.
-// C = 16-byte columns per row (4, 8 or 16).
-template <int C>
-__device__ __forceinline__ int swz(int row, int col) {
-  return col ^ ((row / (16 / C)) & (C - 1));
-}
 
 // Swizzle of row-major Q / dO / K / V tiles that are read both by rows
 // (16-byte reads, 16 consecutive rows per pass) and by the LDS transpose
@@ -329,8 +290,8 @@ __device__ __forceinline__ bool tile_ok(const libra_tile_t &t, int64_t n_q, int6
 // ---------------------------------------------------------------------------
 // Host-side workspace layouts and launchers (defined in attn_fwd.hip / attn_bwd.hip).
 struct FwdLayout {
-  size_t hdr = 0, items = 0, vt = 0, total = 0;
-  int64_t max_items = 0, pitch = 0;
+  size_t hdr = 0, items = 0, total = 0;
+  int64_t max_items = 0;
 };
 struct BwdLayout {
   size_t hdr = 0, ext = 0, gmask = 0, items = 0, qitems = 0, stats = 0, total = 0;
@@ -345,13 +306,11 @@ struct KernelTimer {
   hipEvent_t begin = nullptr, end = nullptr;
 };
 
-// Shared preparation passes (attn_fwd.hip): forward-style work items (also
-// used by the dQ kernel) and the padded transpose of K or V.
+// Shared preparation pass (attn_fwd.hip): forward-style work items, also
+// used by the dQ kernel.
 void enqueue_fwd_items(const int64_t *cu, int64_t n, const libra_tile_t *tiles, int64_t T,
                        int h_q, int h_kv, int64_t n_q, int64_t n_kv, int32_t *hdr,
                        FwdItem *items, int64_t max_items, hipStream_t st);
-void enqueue_transpose(const void *src, const int64_t *cu, int64_t n, int64_t n_kv, int h_kv,
-                       int d, int64_t pitch, void *dst, hipStream_t st);
 int64_t fwd_max_items(int64_t T, int64_t n, int64_t n_q, int h_q, int h_kv);
 
 int launch_fwd(const void *q, const void *k, const void *v, const int64_t *cu, int64_t n,

@@ -7,15 +7,15 @@
 //
 // Kernel structure (one work item = up to 4 query heads of one KV group x 32
 // rows per head, or fewer heads x more rows; 4 waves, one (head, 32 rows) each):
-//   * K blocks of 64 keys and the matching V^T block are staged in LDS,
-//     double-buffered; blocks are anchored at the sample start and only the
-//     row's own sample is visited, so cross-document blocks are never touched.
+//   * K and V blocks of 64 keys are staged in LDS as rows, double-buffered;
+//     blocks are anchored at the sample start and only the row's own sample
+//     is visited, so cross-document blocks are never touched.
 //   * S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (keys on M, queries on N), so
 //     that every lane owns one query: the row max / row sum of the online
 //     softmax are 32 in-lane values plus one exchange with lane ^ 32.
 //   * O^T += V^T P^T with the same instruction; P^T comes straight from the
-//     S^T accumulators (bf16), V^T from a transposed copy of V laid out with
-//     every sample starting on a 64-key boundary (zero padded).
+//     S^T accumulators (bf16), V^T from the row-major V tile through the LDS
+//     transpose reads.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -90,70 +90,20 @@ __global__ __launch_bounds__(kPrepThreads) void prep_fwd_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// V (or K) [n_kv][h_kv][D] -> [h_kv][D][pitch]; sample j occupies
-// [vt_offset(cu[j], j), +ceil64(len)), zero padded past its length.
-template <int D>
-__global__ __launch_bounds__(256) void transpose_v_kernel(const bf16 *__restrict__ v,
-                                                          const int64_t *__restrict__ cu,
-                                                          int64_t n, int64_t n_kv, int h_kv,
-                                                          int64_t pitch, bf16 *__restrict__ vt) {
-  __shared__ bf16 tile[64][D + 2];
-  __shared__ int64_t pos[64];
-  __shared__ int32_t pad_len[64];
-  const int g = blockIdx.y;
-  const int64_t k0 = (int64_t)blockIdx.x * 64;
-  const int tid = threadIdx.x;
-  for (int ci = tid; ci < 64 * D / 2; ci += 256) {
-    const int r = ci / (D / 2), c2 = ci % (D / 2);
-    const int64_t key = k0 + r;
-    uint32_t val = 0;
-    if (key < n_kv)
-      val = *reinterpret_cast<const uint32_t *>(v + ((size_t)key * h_kv + g) * D + 2 * c2);
-    *reinterpret_cast<uint32_t *>(&tile[r][2 * c2]) = val;
-  }
-  if (tid < 64) {
-    const int64_t key = k0 + tid;
-    pos[tid] = -1;
-    pad_len[tid] = 0;
-    if (key < n_kv) {
-      const int64_t j = upper_bound64(cu, n, key) - 1;
-      const int64_t len = cu[j + 1] - cu[j];
-      pos[tid] = vt_offset(cu[j], j) + (key - cu[j]);
-      if (key + 1 == cu[j + 1]) pad_len[tid] = (int32_t)((len + 63) / 64 * 64 - len);
-    }
-  }
-  __syncthreads();
-  for (int e = tid; e < 64 * D; e += 256) {
-    const int dd = e / 64, r = e % 64;
-    if (pos[r] >= 0) vt[((size_t)g * D + dd) * pitch + pos[r]] = tile[r][dd];
-  }
-  for (int r = 0; r < 64; ++r) {
-    if (pad_len[r] == 0) continue;
-    for (int e = tid; e < 64 * D; e += 256) {
-      const int dd = e / 64, p = e % 64;
-      if (p < pad_len[r]) vt[((size_t)g * D + dd) * pitch + pos[r] + 1 + p] = bf16(0.0f);
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
 template <int D>
 struct FwdShape {
-  static constexpr int KC = D / 8;            // 16-byte columns of a K row
-  static constexpr int VC = kFwdBN / 8;       // 16-byte columns of a V^T row
+  static constexpr int KC = D / 8;            // 16-byte columns of a K / V row
   static constexpr int K_EL = kFwdBN * D;
-  static constexpr int V_EL = D * kFwdBN;
-  static constexpr int STAGE = K_EL + V_EL;
-  static constexpr int NK = kFwdBN * KC / 64 / kWaves;   // wave loads of 1 KB per K tile
-  static constexpr int NV = D * VC / 64 / kWaves;        // wave loads per V^T tile
+  static constexpr int STAGE = 2 * K_EL;      // K and V rows of one key block
+  static constexpr int NK = kFwdBN * KC / 64 / kWaves;   // wave loads of 1 KB per tile
   static constexpr size_t SMEM = 2 * STAGE * sizeof(bf16);
 };
 
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
-    const bf16 *__restrict__ q, const bf16 *__restrict__ k, const bf16 *__restrict__ vt,
+    const bf16 *__restrict__ q, const bf16 *__restrict__ k, const bf16 *__restrict__ v,
     const int64_t *__restrict__ cu, const FwdItem *__restrict__ items, int32_t *__restrict__ hdr,
-    int h_q, int h_kv, int64_t n_q, int64_t n_kv, int64_t pitch, float c2,
+    int h_q, int h_kv, int64_t n_q, int64_t n_kv, float c2,
     bf16 *__restrict__ o, float *__restrict__ lse) {
   using S = FwdShape<D>;
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
@@ -162,10 +112,21 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
   int q_serve = blockIdx.x % kXcds, q_left = kXcds;
   // per-lane LDS offsets (elements) of the operand reads, fixed for the kernel
+  // K rows perm32(ln) for S^T; transpose reads of the V tile for the V^T
+  // operand of O^T (rows = keys, as in the dQ kernel's K^T)
   const int prow = perm32(ln);
-  int koff[D / 16], voff_l[4];
-  static_for<D / 16>([&](auto c) { koff[c] = prow * D + 8 * swz<S::KC>(prow, 2 * c + kg); });
-  static_for<4>([&](auto c) { voff_l[c] = prow * kFwdBN + 8 * swz<S::VC>(prow, 2 * c + kg); });
+  int koff[D / 16], troff[D / 32][2];
+  static_for<D / 16>([&](auto c) { koff[c] = prow * D + 8 * swt<S::KC>(prow, 2 * c + kg); });
+  {
+    const int grp = l >> 4, i = (l & 15) >> 2, r = l & 3;
+    static_for<D / 32>([&](auto dt) {
+      static_for<2>([&](auto hf) {
+        const int row = 8 * (grp >> 1) + 4 * hf + i;
+        const int chunk = 4 * dt + 2 * (grp & 1) + (r & 1);
+        troff[dt][hf] = row * D + 8 * swt<S::KC>(row, chunk) + 4 * (r >> 1);
+      });
+    });
+  }
 
   for (;;) {
     if (tid == 0) s_item = take_item(hdr, kFwdQ, q_serve, q_left);
@@ -174,7 +135,6 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     if (idx < 0) break;
     const FwdItem it = items[idx];
     const int64_t key0 = cu[it.sample];
-    const int64_t voff = vt_offset(key0, it.sample);
     const int head = it.head0 + (w % it.nh);
     const int wrow0 = (w / it.nh) * kRows;
     const int wrows = min(max(it.nrows - wrow0, 0), kRows);
@@ -195,25 +155,21 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     static_for<D / 32>([&](auto dt) { static_for<16>([&](auto r) { oacc[dt][int(r)] = 0.f; }); });
     float m_run = -INFINITY, l_run = 0.f;
 
-    // global -> LDS, asynchronous: K block b (keys past the buffer read the
-    // last key instead; they are masked) and the V^T block of the padded copy
+    // global -> LDS, asynchronous: K and V rows of key block b (keys past the
+    // buffer read the last key instead; keys past the row are masked, and
+    // their V rows meet P = 0)
     auto issue = [&](int b, int buf) {
       bf16 *Ks = smem + buf * S::STAGE;
       bf16 *Vs = Ks + S::K_EL;
       static_for<S::NK>([&](auto u) {
         const int wl = w + kWaves * u;
         const int r = wl * (64 / S::KC) + l / S::KC;
-        const int col = swz<S::KC>(r, l % S::KC);
+        const int col = swt<S::KC>(r, l % S::KC);
         int64_t key = key0 + (int64_t)b * kFwdBN + r;
         key = key < n_kv ? key : n_kv - 1;
-        g2l16(k + ((size_t)key * h_kv + it.g) * D + 8 * col, Ks + wl * 512);
-      });
-      static_for<S::NV>([&](auto u) {
-        const int wl = w + kWaves * u;
-        const int r = wl * (64 / S::VC) + l / S::VC;
-        const int col = swz<S::VC>(r, l % S::VC);
-        g2l16(vt + ((size_t)it.g * D + r) * pitch + voff + (int64_t)b * kFwdBN + 8 * col,
-              Vs + wl * 512);
+        const size_t off = ((size_t)key * h_kv + it.g) * D + 8 * col;
+        g2l16(k + off, Ks + wl * 512);
+        g2l16(v + off, Vs + wl * 512);
       });
     };
 
@@ -273,10 +229,12 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
           });
         });
         l_run += ps;
+        // O^T += V^T P^T; key chunk c = 16 keys from tile row 16 c
         static_for<D / 32>([&](auto dt) {
-          const bf16 *vp = Vs + 32 * dt * kFwdBN;
           static_for<4>([&](auto c) {
-            oacc[dt] = mfma32(*reinterpret_cast<const bf16x8 *>(vp + voff_l[c]), pf[c], oacc[dt]);
+            const bf16 *base = Vs + 16 * c * D;
+            oacc[dt] = mfma32(lds_tr16x2(base + troff[dt][0], base + troff[dt][1]), pf[c],
+                              oacc[dt]);
           });
         });
       }
@@ -305,7 +263,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Host launcher.  `ws` is laid out as: header | items | Vt.
+// Host launcher.  `ws` is laid out as: header | items.
 static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 int64_t fwd_max_items(int64_t T, int64_t n, int64_t n_q, int h_q, int h_kv) {
@@ -318,11 +276,9 @@ int64_t fwd_max_items(int64_t T, int64_t n, int64_t n_q, int h_q, int h_kv) {
 FwdLayout fwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, int h_kv, int d) {
   FwdLayout L;
   L.max_items = fwd_max_items(T, n, n_q, h_q, h_kv);
-  L.pitch = vt_pitch(n_kv, n);
   L.hdr = 0;
   L.items = align256(kHdrSlots * sizeof(int32_t));
-  L.vt = align256(L.items + (size_t)L.max_items * sizeof(FwdItem));
-  L.total = align256(L.vt + (size_t)h_kv * d * L.pitch * sizeof(bf16));
+  L.total = align256(L.items + (size_t)L.max_items * sizeof(FwdItem));
   return L;
 }
 
@@ -333,7 +289,6 @@ static int launch_fwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const int64
                         char *ws, const FwdLayout &L, hipStream_t st, const KernelTimer *tm) {
   int32_t *hdr = reinterpret_cast<int32_t *>(ws + L.hdr);
   FwdItem *items = reinterpret_cast<FwdItem *>(ws + L.items);
-  bf16 *vt = reinterpret_cast<bf16 *>(ws + L.vt);
   static bool attr_set = false;
   if (!attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_fwd_kernel<D>),
@@ -344,14 +299,12 @@ static int launch_fwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const int64
   }
   hipLaunchKernelGGL(prep_fwd_kernel, dim3(1), dim3(kPrepThreads), 0, st, cu, n, tiles, T, h_q,
                      h_kv, n_q, n_kv, hdr, items, L.max_items);
-  hipLaunchKernelGGL(transpose_v_kernel<D>, dim3((unsigned)((n_kv + 63) / 64), h_kv), dim3(256),
-                     0, st, v, cu, n, n_kv, h_kv, L.pitch, vt);
   int dev = 0, cus = 256;
   hipGetDevice(&dev);
   hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (tm) hipEventRecord(tm->begin, st);
   hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3(cus * 2), dim3(kThreads), FwdShape<D>::SMEM, st, q,
-                     k, vt, cu, items, hdr, h_q, h_kv, n_q, n_kv, L.pitch, scale * kLog2e, o,
+                     k, v, cu, items, hdr, h_q, h_kv, n_q, n_kv, scale * kLog2e, o,
                      lse);
   if (tm) hipEventRecord(tm->end, st);
   const hipError_t e = hipGetLastError();
@@ -364,19 +317,6 @@ void enqueue_fwd_items(const int64_t *cu, int64_t n, const libra_tile_t *tiles, 
                        FwdItem *items, int64_t max_items, hipStream_t st) {
   hipLaunchKernelGGL(prep_fwd_kernel, dim3(1), dim3(kPrepThreads), 0, st, cu, n, tiles, T, h_q,
                      h_kv, n_q, n_kv, hdr, items, max_items);
-}
-
-void enqueue_transpose(const void *src, const int64_t *cu, int64_t n, int64_t n_kv, int h_kv,
-                       int d, int64_t pitch, void *dst, hipStream_t st) {
-  const dim3 grid((unsigned)((n_kv + 63) / 64), h_kv);
-  if (d == 128)
-    hipLaunchKernelGGL(transpose_v_kernel<128>, grid, dim3(256), 0, st,
-                       static_cast<const bf16 *>(src), cu, n, n_kv, h_kv, pitch,
-                       static_cast<bf16 *>(dst));
-  else
-    hipLaunchKernelGGL(transpose_v_kernel<64>, grid, dim3(256), 0, st,
-                       static_cast<const bf16 *>(src), cu, n, n_kv, h_kv, pitch,
-                       static_cast<bf16 *>(dst));
 }
 
 int launch_fwd(const void *q, const void *k, const void *v, const int64_t *cu, int64_t n,
