@@ -644,20 +644,22 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
       });
     };
 
-    int issued = 0;
-    for (; issued < nkb && issued < S::NSTAGE - 1; ++issued) issue(issued, issued);
-    for (int b = 0; b < nkb; ++b) {
-      // this block's loads are complete once at most (issued - 1 - b) later
-      // blocks are outstanding; then every wave's part is in LDS
-      wait_stages<S::LOADS, S::NSTAGE - 2>(issued - 1 - b);
+    // key blocks go in pairs: pair p = blocks 2p, 2p + 1 in stages 2 (p % 2)
+    // and 2 (p % 2) + 1; the loads of pair p + 1 overlap the compute of pair p
+    const int npairs = (nkb + 1) / 2;
+    auto issue_pair = [&](int p) {
+      issue(2 * p, 2 * (p & 1));
+      if (2 * p + 1 < nkb) issue(2 * p + 1, 2 * (p & 1) + 1);
+    };
+    issue_pair(0);
+    for (int p = 0; p < npairs; ++p) {
+      wait_vm_n<0>();             // pair p, the only loads in flight
       barrier_nofence();
-      // the stage of block b - 1 is free again (every wave passed the barrier)
-      if (issued < nkb) {
-        issue(issued, issued % S::NSTAGE);
-        ++issued;
-      }
+      // the stages of pair p - 1 are free again (every wave passed the barrier)
+      if (p + 1 < npairs) issue_pair(p + 1);
+      for (int b = 2 * p; b < 2 * p + 2 && b < nkb; ++b) {
       if (b < wave_nkb) {
-        const bf16 *Ks = smem + (b % S::NSTAGE) * S::STAGE;
+        const bf16 *Ks = smem + (2 * (p & 1) + (b & 1)) * S::STAGE;
         const bf16 *Vs = Ks + S::K_EL;
         f32x16 s[2], dp[2];
         static_for<2>([&](auto t) {
@@ -696,6 +698,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
           });
         });
         sched_pipeline<4 * (D / 32), 4>();
+      }
       }
     }
     wait_vm_n<0>();
