@@ -296,11 +296,12 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
       });
     });
   }
-  // per-lane parts of the staging addresses (elements), fixed for the kernel
-  int q_lane[S::NQ];
+  // per-lane parts of the staging addresses (bytes), fixed for the kernel
+  static_assert(S::NQ == 1 || S::NQ == 2, "two or four staging copies per head");
+  uint32_t q_lane[S::NQ];
   static_for<S::NQ>([&](auto u) {
     const int r = (w + kWaves * u) * (64 / S::QC) + l / S::QC;
-    q_lane[u] = r * h_q * D + 8 * swt<S::QC>(r, l % S::QC);
+    q_lane[u] = 2u * (uint32_t)(r * h_q * D + 8 * swt<S::QC>(r, l % S::QC));
   });
 
   for (;;) {
@@ -350,11 +351,13 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
         bf16 *Fs = dOs + S::Q_EL;
         const int64_t qo = st.qoff + (hb ? dq2 : 0);
         if (!st.clamp()) {
-          static_for<S::NQ>([&](auto u) {
-            const int wl = w + kWaves * u;
-            g2l16(q + qo + q_lane[u], Qs + wl * 512);
-            g2l16(dout + qo + q_lane[u], dOs + wl * 512);
-          });
+          // wave w stages rows w * 64 / QC ... of each 16-byte column group;
+          // wave loads u = 0, 1 land 1 KiB x (w + 4 u) into the tile
+          const uint32_t lq = lds_addr(Qs) + 1024u * w, ld = lds_addr(dOs) + 1024u * w;
+          if constexpr (S::NQ == 2)
+            g2l16x4(q + qo, dout + qo, q_lane[0], q_lane[1], lq, lq + 4096u, ld, ld + 4096u);
+          else
+            g2l16x2(q + qo, dout + qo, q_lane[0], lq, ld);
         } else {
           // the last block of the buffer: rows past it read the last row (masked)
           const int64_t m0 = st.m0();
@@ -469,17 +472,27 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
       });
     };
 
+    // Steps are walked once, at issue; what the compute side needs of the step
+    // in ring stage j (lo | hi << 8 | two << 16, and the q_loc of the block's
+    // row 0) waits in lane j of desc / desc_qb.
     StepIter iss{tiles, T, n_q, n_kv, key0, len, h_q, g, G, kloc0, D, nblk};
     iss.start();
-    StepIter cur = iss;
+    int desc = 0, desc_qb = 0;
     int issued = 0, computed = 0;
-    while (cur.valid) {
-      // keep up to NSTAGE - 1 steps in flight, the one computed now included
-      while (iss.valid && issued < computed + S::NSTAGE - 1) {
-        issue(iss, issued & (S::NSTAGE - 1));
-        iss.next();
-        ++issued;
+    auto issue_next = [&]() {
+      const int sg = issued & (S::NSTAGE - 1);
+      issue(iss, sg);
+      if (l == sg) {
+        desc = iss.lo() | iss.hi() << 8 | (iss.two() ? 1 << 16 : 0);
+        desc_qb = iss.qb();
       }
+      iss.next();
+      ++issued;
+    };
+    while (iss.valid && issued < S::NSTAGE - 1) issue_next();
+    while (computed < issued) {
+      // keep up to NSTAGE - 1 steps in flight, the one computed now included
+      if (iss.valid && issued < computed + S::NSTAGE - 1) issue_next();
       // wait for this step's loads: in steady state NSTAGE - 2 later steps
       // stay in flight; near the end of an item, wait for everything
       if (issued - 1 - computed >= S::NSTAGE - 2) {
@@ -490,11 +503,13 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
       }
       barrier_nofence();
 
-      const int lo_l = cur.lo(), hi_l = cur.hi();
-      const int qb = cur.qb();                                  // q_loc of the block's row 0
+      const int sg = computed & (S::NSTAGE - 1);
+      const int dsc = __builtin_amdgcn_readlane(desc, sg);
+      const int lo_l = dsc & 0xff, hi_l = (dsc >> 8) & 0xff;
+      const bool two = (dsc >> 16) != 0;
+      const int qb = __builtin_amdgcn_readlane(desc_qb, sg);   // q_loc of the block's row 0
       if (kw0 <= qb + hi_l - 1) {
-        const bf16 *Qs = smem + (computed & (S::NSTAGE - 1)) * S::STAGE_EL;
-        const bool two = cur.two();
+        const bf16 *Qs = smem + sg * S::STAGE_EL;
         // interior blocks: every row inside the fragment and at or after every key
         const bool full = lo_l == 0 && hi_l == kRows && wave_keys_ok && kw0 + 31 <= qb;
         const int need = kl - qb;                               // first iq with q_loc >= kl
@@ -504,7 +519,6 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
         if (two) step(full, Qs + S::HEAD_EL, lower, upper);
       }
       ++computed;
-      cur.next();
     }
 
     // ---- write dK, dV for this wave's 32 keys

@@ -205,6 +205,53 @@ __device__ __forceinline__ void g2l16(const void *g, bf16 *lds) {
       : "v"(g), "s"(a)
       : "memory");
 }
+// LDS byte address of a shared-memory pointer, as a wave-uniform value.
+__device__ __forceinline__ uint32_t lds_addr(const bf16 *lds) {
+  return __builtin_amdgcn_readfirstlane(
+      (uint32_t)(size_t)(__attribute__((address_space(3))) const bf16 *)lds);
+}
+// Four 16-byte-per-lane global -> LDS copies in one statement (one M0 save and
+// restore): rows at byte offsets o0, o1 (per lane) from the wave-uniform bases
+// ga and gb land at LDS addresses la0, la1 (from ga) and lb0, lb1 (from gb).
+__device__ __forceinline__ void g2l16x4(const void *ga, const void *gb, uint32_t o0, uint32_t o1,
+                                        uint32_t la0, uint32_t la1, uint32_t lb0, uint32_t lb1) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %7\n\t"
+      "s_mov_b32 m0, %4\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, %7\n\t"
+      "s_mov_b32 m0, %5\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %8\n\t"
+      "s_mov_b32 m0, %6\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, %8\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(o0), "v"(o1), "s"(la0), "s"(la1), "s"(lb0), "s"(lb1), "s"(ga), "s"(gb)
+      : "memory");
+}
+// Two such copies: the row at o0 from ga to la0 and from gb to lb0.
+__device__ __forceinline__ void g2l16x2(const void *ga, const void *gb, uint32_t o0,
+                                        uint32_t la0, uint32_t lb0) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %4\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %5\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(o0), "s"(la0), "s"(lb0), "s"(ga), "s"(gb)
+      : "memory");
+}
 // Workgroup barrier without the memory fence of __syncthreads(): the fence
 // would wait for every outstanding global load of the wave, including the
 // global -> LDS prefetches of later pipeline stages.  Callers make the data
