@@ -101,14 +101,33 @@ __global__ __launch_bounds__(kPrepThreads) void prep_bwd_kernel(
 // Pre-pass over the covered (row, head) pairs, 32 rows at a time: per 32-row
 // block of each head the 32 values LSE * log2(e) followed by the 32 values
 // D = rowsum(dO * O) ("stats", [h_q][nq_pad / 32][64] floats, so one
-// 256-byte load fetches both).
+// 256-byte load fetches both), and for the dK / dV kernel the same two
+// quantities as one extra 16-deep k-block of the S and dP products ("aug",
+// [h_q][nq_pad / 32][2][64 lanes][8] bf16): MFMA A-operand lane l < 32 holds
+// three bf16 terms summing to -LSE / scale (first record) or -D (second) of
+// the block's row perm32(l), then zeros; lanes 32..63 hold zeros.  Against a
+// B operand of ones in k = 0, 1, 2 the products then come out as S - LSE / scale
+// and dP - D directly.
 constexpr int kTileSplit = 64;
+constexpr int kAugEl = 2 * 64 * 8;   // bf16 elements of one block's two records
+
+// x as hi + mid + lo, three bf16 values (exact to about 2^-24 |x|).
+__device__ __forceinline__ void split3(float x, bf16x8 &r) {
+  const bf16 a = static_cast<bf16>(x);
+  const float x1 = x - static_cast<float>(a);
+  const bf16 b = static_cast<bf16>(x1);
+  const bf16 c = static_cast<bf16>(x1 - static_cast<float>(b));
+  static_for<8>([&](auto i) { r[int(i)] = bf16(0.f); });
+  r[0] = a;
+  r[1] = b;
+  r[2] = c;
+}
 
 template <int D>
 __global__ __launch_bounds__(256) void bwd_pre_kernel(
     const bf16 *__restrict__ o, const bf16 *__restrict__ dout, const float *__restrict__ lse,
     const libra_tile_t *__restrict__ tiles, int h_q, int64_t n_q, int64_t n_kv,
-    int64_t nq_pad, float *__restrict__ stats) {
+    int64_t nq_pad, float scale, float *__restrict__ stats, bf16 *__restrict__ aug) {
   const int tid = threadIdx.x;
   const libra_tile_t tl = tiles[blockIdx.x / kTileSplit];
   if (!tile_ok(tl, n_q, n_kv, h_q)) return;
@@ -135,8 +154,15 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(
       acc += __shfl_xor(acc, 4);
       if (part == 0 && ok) {
         float *st = stats + ((size_t)h * (nq_pad / kRows) + m) * 2 * kRows;
-        st[r] = lse[(size_t)h * n_q + row] * kLog2e;
+        const float lv = lse[(size_t)h * n_q + row];
+        st[r] = lv * kLog2e;
         st[kRows + r] = acc;
+        bf16 *ag = aug + ((size_t)h * (nq_pad / kRows) + m) * kAugEl + 8 * perm32(r);
+        bf16x8 sv, dv;
+        split3(-lv / scale, sv);
+        split3(-acc, dv);
+        *reinterpret_cast<bf16x8 *>(ag) = sv;
+        *reinterpret_cast<bf16x8 *>(ag + kAugEl / 2) = dv;
       }
     }
   }
@@ -154,15 +180,15 @@ template <int D>
 struct KvShape {
   static constexpr int QC = D / 8;          // 16-byte columns of a Q / dO row
   static constexpr int Q_EL = kRows * D;
-  static constexpr int F_EL = 2 * 2 * kRows;                 // 64 floats as bf16 slots
-  static constexpr int HEAD_EL = 2 * Q_EL + F_EL;             // Q, dO, stats of one head
+  static constexpr int F_EL = kAugEl;                         // the two augmented operands
+  static constexpr int HEAD_EL = 2 * Q_EL + F_EL;             // Q, dO, aug of one head
   static constexpr int STAGE_EL = 2 * HEAD_EL;                // a step is two query heads
   static constexpr int NSTAGE = 4;                            // LDS ring of steps
   static_assert((NSTAGE & (NSTAGE - 1)) == 0, "ring index by mask");
   static constexpr int NQ = kRows * QC / 64 / kWaves;   // wave loads per Q (dO) tile
-  static constexpr int LOADS = 4 * NQ;                  // per wave per step (+1 on waves 0, 1)
+  static constexpr int LOADS = 4 * NQ + 1;              // per wave per step
   static constexpr size_t SMEM = NSTAGE * STAGE_EL * sizeof(bf16);
-  static_assert((NSTAGE - 2) * (LOADS + 1) <= 63, "vmcnt range");
+  static_assert((NSTAGE - 2) * LOADS <= 63, "vmcnt range");
 };
 
 // s_waitcnt vmcnt(N) for a compile-time N.
@@ -188,7 +214,7 @@ __device__ __forceinline__ void wait_stages(int k) {
 // tiles in list order, query blocks in row order, heads in order.  Per
 // fragment (one tile's rows of the sample) everything a step needs is
 // precomputed, so that advancing is a few 32-bit scalar operations plus two
-// running 64-bit offsets (the Q / dO element offset and the stats offset).
+// running 64-bit offsets (the Q / dO element offset and the aug offset).
 struct StepIter {
   const libra_tile_t *tiles;
   int64_t T, n_q, n_kv, key0, len;
@@ -201,7 +227,7 @@ struct StepIter {
   bool clamp_last;          // the last block runs past the end of the buffer
   // position
   int mi, h;
-  int64_t qoff, soff;       // element offset of (row0 + 32 mi, h) in Q / dO; stats offset
+  int64_t qoff, soff;       // element offset of (row0 + 32 mi, h) in Q / dO; in aug
   bool valid;
 
   __device__ bool seek() {
@@ -229,7 +255,7 @@ struct StepIter {
       mi = 0;
       h = h0;
       qoff = (row0 * h_q + h0) * D;
-      soff = ((int64_t)h0 * nblk + mf) * 64;
+      soff = ((int64_t)h0 * nblk + mf) * kAugEl;
       return true;
     }
     return false;
@@ -240,14 +266,14 @@ struct StepIter {
   __device__ void next() {
     if ((h += 2) < h1) {
       qoff += 2 * D;
-      soff += 2 * nblk * 64;
+      soff += 2 * nblk * kAugEl;
       return;
     }
     const int back = h - 2 - h0;                 // heads advanced within this block
     h = h0;
     if (++mi < nm) {
       qoff += (int64_t)(kRows * h_q - back) * D;
-      soff -= (int64_t)back * nblk * 64 - 64;
+      soff -= (int64_t)back * nblk * kAugEl - kAugEl;
       return;
     }
     ++t;
@@ -264,7 +290,7 @@ struct StepIter {
 template <int D>
 __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) void attn_bwd_dkdv_kernel(
     const bf16 *__restrict__ k, const bf16 *__restrict__ v, const bf16 *__restrict__ q,
-    const bf16 *__restrict__ dout, const float *__restrict__ stats,
+    const bf16 *__restrict__ dout, const bf16 *__restrict__ aug,
     const int64_t *__restrict__ cu, const libra_tile_t *__restrict__ tiles, int64_t T,
     const BwdItem *__restrict__ items, int32_t *__restrict__ hdr, int h_q, int h_kv,
     int64_t n_q, int64_t n_kv, int64_t nq_pad, float scale, float c2,
@@ -303,6 +329,9 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
     const int r = (w + kWaves * u) * (64 / S::QC) + l / S::QC;
     q_lane[u] = 2u * (uint32_t)(r * h_q * D + 8 * swt<S::QC>(r, l % S::QC));
   });
+  // B operand of the augmented k-block: ones in k = 0, 1, 2 (lanes of kg 0)
+  bf16x8 ones3;
+  static_for<8>([&](auto i) { ones3[int(i)] = bf16(kg == 0 && i < 3 ? 1.f : 0.f); });
 
   for (;;) {
     if (tid == 0) s_item = take_item(hdr, kBwdQ, q_serve, q_left);
@@ -337,18 +366,17 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
       dka[dt] = mfma_zero();
     });
 
-    // ---- one step = (32-row query block, head); its Q, dO rows and stats go
+    // ---- one step = (32-row query block, head); its Q, dO rows and aug go
     // global -> LDS into ring stage `sg` (rows of the block outside the
     // fragment are real rows of other fragments or the clamped last row;
     // their P and dS are masked to zero)
     auto issue = [&](const StepIter &st, int sg) {
       // head h into the first half of the stage, head h + 1 (or h again when
       // the step has one head; it is then not computed) into the second
-      const int64_t dq2 = st.two() ? D : 0, ds2 = st.two() ? nblk * 64 : 0;
+      const int64_t dq2 = st.two() ? D : 0, ds2 = st.two() ? nblk * kAugEl : 0;
       static_for<2>([&](auto hb) {
         bf16 *Qs = smem + sg * S::STAGE_EL + hb * S::HEAD_EL;
         bf16 *dOs = Qs + S::Q_EL;
-        bf16 *Fs = dOs + S::Q_EL;
         const int64_t qo = st.qoff + (hb ? dq2 : 0);
         if (!st.clamp()) {
           // wave w stages rows w * 64 / QC ... of each 16-byte column group;
@@ -371,8 +399,12 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
             g2l16(dout + off, dOs + wl * 512);
           });
         }
-        if (w == hb && l < 16) g2l16(stats + st.soff + (hb ? ds2 : 0) + 4 * l, Fs);
       });
+      // one augmented record per wave: head w / 2, record w % 2
+      const int64_t ao = st.soff + (w >= 2 ? ds2 : 0) + (w & 1) * (kAugEl / 2);
+      g2l16s(aug + ao, 16u * l,
+             lds_addr(smem + sg * S::STAGE_EL + (w >> 1) * S::HEAD_EL + 2 * S::Q_EL +
+                      (w & 1) * (kAugEl / 2)));
     };
 
     // ---- compute one step from the LDS stage at Qs.  Rows of the block are
@@ -381,43 +413,37 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
     auto step = [&](bool full, const bf16 *Qs, int lower, int upper) {
       constexpr int NC = D / 16, NT = D / 32;
       const bf16 *dOs = Qs + S::Q_EL;
-      const float *l2s = reinterpret_cast<const float *>(dOs + S::Q_EL);
-      const float *dvs = l2s + kRows;
-      // (1) Q rows and the LSE values of this lane's rows
-      bf16x8 qa[NC], oa[NC];
-      f32x4 l2v[4], ddv[4];
+      const bf16 *Ag = dOs + S::Q_EL;     // -LSE / scale record, then the -D record
+      // (1) Q rows and this lane's part of the -LSE / scale operand
+      bf16x8 qa[NC], oa[NC], sag, dag;
+      sag = *reinterpret_cast<const bf16x8 *>(Ag + 8 * l);
       static_for<NC>([&](auto c) { qa[c] = *reinterpret_cast<const bf16x8 *>(Qs + qoff[c]); });
-      static_for<4>([&](auto j) {
-        l2v[j] = *reinterpret_cast<const f32x4 *>(l2s + 16 * (j >> 1) + 8 * kg + 4 * (j & 1));
-      });
       __builtin_amdgcn_sched_barrier(0);
-      // (2) S = Q K^T (queries on M, this lane's key on N) while dO rows and
-      // the D values load
-      f32x16 sa = mfma_zero_c(), pa;
+      // (2) S - LSE / scale = [Q | aug] [K | ones]^T (queries on M, this
+      // lane's key on N) while the dO rows and the -D operand load
+      f32x16 sa = mfma32(sag, ones3, mfma_zero_c()), pa;
       static_for<NC>([&](auto c) { sa = mfma32(qa[c], kf[c], sa); });
+      dag = *reinterpret_cast<const bf16x8 *>(Ag + kAugEl / 2 + 8 * l);
       static_for<NC>([&](auto c) { oa[c] = *reinterpret_cast<const bf16x8 *>(dOs + qoff[c]); });
-      static_for<4>([&](auto j) {
-        ddv[j] = *reinterpret_cast<const f32x4 *>(dvs + 16 * (j >> 1) + 8 * kg + 4 * (j & 1));
-      });
-      static_for<NC>([&](auto i) {
+      static_for<NC + 1>([&](auto i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, i < 6 ? 2 : 0, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, i < NC / 2 + 1 ? 2 : 0, 0);
       });
       __builtin_amdgcn_sched_barrier(0);
-      // (3) dP = dO V^T with P = exp2(S c2 - LSE log2 e) on the VALU and the
-      // transpose reads of dO^T; register 8 hh + i of S holds row 16 hh + 8 kg + i
+      // (3) dP - D = [dO | aug] [V | ones]^T with P = exp2((S - LSE / scale) c2)
+      // on the VALU and the transpose reads of dO^T; register 8 hh + i of S
+      // holds row 16 hh + 8 kg + i
       bf16x8 ta[NT][2];
       float pf[16];
       bf16x8 pb16[2], db16[2];
       auto phase3 = [&](auto mask_t) {
       constexpr bool MASK = decltype(mask_t)::value;
-      pa = mfma_zero_c();
+      pa = mfma32(dag, ones3, mfma_zero_c());
       static_for<NC>([&](auto c) { pa = mfma32(oa[c], vf[c], pa); });
       static_for<2>([&](auto hh) {
         static_for<8>([&](auto i) {
           constexpr int r = 8 * hh + i;
-          const float l2 = l2v[2 * hh + (i >> 2)][int(i) & 3];
-          float p = fast_exp2(__builtin_fmaf(sa[r], c2, -l2));
+          float p = fast_exp2(sa[r] * c2);
           if constexpr (MASK) {
             const int iq = 16 * hh + 8 * kg + i;
             p = (iq >= lower && iq < upper) ? p : 0.f;
@@ -432,10 +458,10 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
           ta[dt][c] = lds_tr16x2(base + troff[dt][0], base + troff[dt][1]);
         });
       });
-      static_for<NC>([&](auto i) {
+      static_for<NC + 1>([&](auto i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, MASK ? 10 : 7, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, MASK ? 9 : 5, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, i < NC ? 2 : 0, 0);
       });
       };
       if (full) phase3(std::false_type{});
@@ -450,8 +476,7 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
       static_for<2>([&](auto hh) {
         static_for<8>([&](auto i) {
           constexpr int r = 8 * hh + i;
-          const float dd = ddv[2 * hh + (i >> 2)][int(i) & 3];
-          db16[hh][int(i)] = static_cast<bf16>(pf[r] * (pa[r] - dd));
+          db16[hh][int(i)] = static_cast<bf16>(pf[r] * pa[r]);
         });
       });
       static_for<NT>([&](auto dt) {
@@ -496,8 +521,7 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
       // wait for this step's loads: in steady state NSTAGE - 2 later steps
       // stay in flight; near the end of an item, wait for everything
       if (issued - 1 - computed >= S::NSTAGE - 2) {
-        if (w < 2) wait_vm_n<(S::NSTAGE - 2) * (S::LOADS + 1)>();
-        else wait_vm_n<(S::NSTAGE - 2) * S::LOADS>();
+        wait_vm_n<(S::NSTAGE - 2) * S::LOADS>();
       } else {
         wait_vm_n<0>();
       }
@@ -747,7 +771,8 @@ BwdLayout bwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, i
   L.items = align256b(L.gmask + (size_t)n * sizeof(unsigned long long));
   L.qitems = align256b(L.items + (size_t)L.max_items * sizeof(BwdItem));
   L.stats = align256b(L.qitems + (size_t)L.max_qitems * sizeof(FwdItem));
-  L.total = align256b(L.stats + (size_t)h_q * L.nq_pad * 2 * sizeof(float));
+  L.aug = align256b(L.stats + (size_t)h_q * L.nq_pad * 2 * sizeof(float));
+  L.total = align256b(L.aug + (size_t)h_q * (L.nq_pad / kRows) * kAugEl * sizeof(bf16));
   return L;
 }
 
@@ -764,6 +789,7 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
   BwdItem *items = reinterpret_cast<BwdItem *>(ws + L.items);
   FwdItem *qitems = reinterpret_cast<FwdItem *>(ws + L.qitems);
   float *stats = reinterpret_cast<float *>(ws + L.stats);
+  bf16 *aug = reinterpret_cast<bf16 *>(ws + L.aug);
   static bool attr_set = false;
   if (!attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_bwd_dkdv_kernel<D>),
@@ -786,20 +812,20 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
                        h_kv, n_q, n_kv, hdr, ext, gmask, items, L.max_items);
     enqueue_fwd_items(cu, n, tiles, T, h_q, h_kv, n_q, n_kv, hdr, qitems, L.max_qitems, st);
     {
-      // stats of rows outside the covered ones stay zero (finite): they are
-      // only read for masked rows
-      const int64_t s16 = (int64_t)h_q * L.nq_pad * 2 * (int64_t)sizeof(float) / 16;
+      // stats and aug of rows outside the covered ones stay zero (finite):
+      // they are only read for masked rows; lanes 32..63 of aug stay zero
+      const int64_t s16 = (int64_t)(L.total - L.stats) / 16;
       hipLaunchKernelGGL(zero_kernel, dim3((unsigned)std::min<int64_t>((s16 + 255) / 256, 4096)),
                          dim3(256), 0, st, reinterpret_cast<uint4 *>(stats), s16);
     }
     hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)(T * kTileSplit)), dim3(256), 0, st, o,
-                       dout, lse, tiles, h_q, n_q, n_kv, L.nq_pad, stats);
+                       dout, lse, tiles, h_q, n_q, n_kv, L.nq_pad, scale, stats, aug);
     int dev = 0, cus = 256;
     hipGetDevice(&dev);
     hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (tm_kv) hipEventRecord(tm_kv->begin, st);
     hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(cus), dim3(kThreads), KvShape<D>::SMEM, st, k,
-                       v, q, dout, stats, cu, tiles, T, items, hdr, h_q, h_kv, n_q, n_kv,
+                       v, q, dout, aug, cu, tiles, T, items, hdr, h_q, h_kv, n_q, n_kv,
                        L.nq_pad, scale, scale * kLog2e, dk, dv, accumulate ? 1 : 0);
     if (tm_kv) hipEventRecord(tm_kv->end, st);
     if (tm_q) hipEventRecord(tm_q->begin, st);

@@ -235,6 +235,20 @@ __device__ __forceinline__ void g2l16x4(const void *ga, const void *gb, uint32_t
       : "v"(o0), "v"(o1), "s"(la0), "s"(la1), "s"(lb0), "s"(lb1), "s"(ga), "s"(gb)
       : "memory");
 }
+// One such copy: lane bytes at byte offset o from the wave-uniform base g land
+// at LDS address la.
+__device__ __forceinline__ void g2l16s(const void *g, uint32_t o, uint32_t la) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %3\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(o), "s"(la), "s"(g)
+      : "memory");
+}
 // Two such copies: the row at o0 from ga to la0 and from gb to lb0.
 __device__ __forceinline__ void g2l16x2(const void *ga, const void *gb, uint32_t o0,
                                         uint32_t la0, uint32_t lb0) {
@@ -341,7 +355,7 @@ struct FwdLayout {
   int64_t max_items = 0;
 };
 struct BwdLayout {
-  size_t hdr = 0, ext = 0, gmask = 0, items = 0, qitems = 0, stats = 0, total = 0;
+  size_t hdr = 0, ext = 0, gmask = 0, items = 0, qitems = 0, stats = 0, aug = 0, total = 0;
   int64_t max_items = 0, max_qitems = 0, nq_pad = 0;
 };
 
