@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OUT_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "liblibra.so")
 
-HIP_SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "attn_api.hip"]
+HIP_SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "attn_bwd_dq.hip", "attn_api.hip"]
 CXX_SOURCES = ["plan.cpp", "vrsp.cpp"]
 ARCH = os.environ.get("LIBRA_OFFLOAD_ARCH", "gfx950")
 
@@ -30,14 +30,17 @@ def _hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-# Per-source extra flags.  The forward kernel keeps its MFMA accumulators in
-# VGPRs (two workgroups per CU; the default heuristic shuffles them through
-# AGPRs inside the hot loop).  The backward kernels keep the long-lived dK /
-# dV / dQ accumulators in AGPRs, which is the default form once they are
-# initialised by an MFMA, and leaves the 256 VGPRs to the operands in flight.
+# Per-source extra flags.  The forward kernel takes its MFMA results in VGPRs
+# (two workgroups per CU; the default heuristic shuffles its accumulators
+# through AGPRs inside the hot loop).  The backward kernels keep their
+# long-lived dK / dV / dQ accumulators in AGPRs, the default form once they
+# are initialised by an MFMA, which leaves the 256 VGPRs to the operands in
+# flight (in VGPR form the dQ kernel runs out of registers for its LDS reads
+# and serialises them).
+_VGPR_FORM = ["-mllvm", "--amdgpu-mfma-vgpr-form=1"]
 EXTRA_FLAGS = {
-    "attn_fwd.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1"],
-    "attn_api.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1"],
+    "attn_fwd.hip": _VGPR_FORM,
+    "attn_api.hip": _VGPR_FORM,
 }
 
 

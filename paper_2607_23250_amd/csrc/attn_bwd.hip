@@ -15,7 +15,7 @@
 //     dK^T = Q^T dS need; the dO^T / Q^T operands come from the same
 //     row-major LDS tiles through the LDS transpose reads.  Query blocks are
 //     staged in an LDS ring, up to seven ahead of the one computed.
-//   * dQ, query-stationary, shaped like the forward: S^T = K Q^T and
+//   * dQ (attn_bwd_dq.hip), query-stationary, shaped like the forward: S^T = K Q^T and
 //     dP^T = V dO^T (lane = query), dS^T = P^T * (dP^T - D), then
 //     dQ^T += K^T dS^T; key blocks are staged in a 4-deep LDS ring.  It recomputes S and dP instead of accumulating dQ
 //     across key blocks with atomics: on long samples that accumulation is
@@ -111,17 +111,6 @@ __global__ __launch_bounds__(kPrepThreads) void prep_bwd_kernel(
 constexpr int kTileSplit = 64;
 constexpr int kAugEl = 2 * 64 * 8;   // bf16 elements of one block's two records
 
-// x as hi + mid + lo, three bf16 values (exact to about 2^-24 |x|).
-__device__ __forceinline__ void split3(float x, bf16x8 &r) {
-  const bf16 a = static_cast<bf16>(x);
-  const float x1 = x - static_cast<float>(a);
-  const bf16 b = static_cast<bf16>(x1);
-  const bf16 c = static_cast<bf16>(x1 - static_cast<float>(b));
-  static_for<8>([&](auto i) { r[int(i)] = bf16(0.f); });
-  r[0] = a;
-  r[1] = b;
-  r[2] = c;
-}
 
 template <int D>
 __global__ __launch_bounds__(256) void bwd_pre_kernel(
@@ -190,25 +179,6 @@ struct KvShape {
   static constexpr size_t SMEM = NSTAGE * STAGE_EL * sizeof(bf16);
   static_assert((NSTAGE - 2) * LOADS <= 63, "vmcnt range");
 };
-
-// s_waitcnt vmcnt(N) for a compile-time N.
-template <int N>
-__device__ __forceinline__ void wait_vm_n() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-// Wait until at most k * L vector-memory operations are outstanding
-// (k in [0, KMAX]; larger k wait for KMAX * L).
-template <int L, int KMAX>
-__device__ __forceinline__ void wait_stages(int k) {
-  bool done = false;
-  static_for<KMAX>([&](auto i) {
-    if (!done && k == int(i)) {
-      wait_vm_n<int(i) * L>();
-      done = true;
-    }
-  });
-  if (!done) wait_vm_n<KMAX * L>();
-}
 
 // Walks the steps (32-row query block x query head) that attend one KV block:
 // tiles in list order, query blocks in row order, heads in order.  Per
@@ -582,182 +552,6 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
 }
 
 // ---------------------------------------------------------------------------
-// dQ kernel (query-stationary; work items are the forward's).
-template <int D>
-struct DqShape {
-  static constexpr int KC = D / 8;            // 16-byte columns of a K / V row
-  static constexpr int K_EL = kFwdBN * D;
-  static constexpr int STAGE = 2 * K_EL;
-  static constexpr int NSTAGE = 4;            // LDS ring of key blocks
-  static constexpr int NK = kFwdBN * KC / 64 / kWaves;   // wave loads per K (V) tile
-  static constexpr int LOADS = 2 * NK;                    // per wave per block
-  static constexpr size_t SMEM = NSTAGE * STAGE * sizeof(bf16);
-  static_assert((NSTAGE - 1) * LOADS <= 63, "vmcnt range");
-};
-
-template <int D>
-__global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
-    const bf16 *__restrict__ q, const bf16 *__restrict__ dout, const bf16 *__restrict__ k,
-    const bf16 *__restrict__ v, const float *__restrict__ stats,
-    const int64_t *__restrict__ cu, const FwdItem *__restrict__ items,
-    int32_t *__restrict__ hdr, int h_q, int h_kv, int64_t n_q, int64_t n_kv, int64_t nq_pad,
-    float c2, float scale, bf16 *__restrict__ dq) {
-  using S = DqShape<D>;
-  extern __shared__ __attribute__((aligned(16))) bf16 smem[];
-  __shared__ int32_t s_item;
-  const int tid = threadIdx.x, l = tid & 63, ln = l & 31, kg = l >> 5;
-  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
-  int q_serve = blockIdx.x % kXcds, q_left = kXcds;
-  // per-lane LDS offsets (elements): K / V rows perm32(ln) for S^T and dP^T,
-  // and the transpose reads of the K tile that give the K^T operand of dQ^T
-  // (as in the dK/dV kernel, with keys in place of query rows)
-  const int prow = perm32(ln);
-  int koff[D / 16], troff[D / 32][2];
-  static_for<D / 16>([&](auto c) { koff[c] = prow * D + 8 * swt<S::KC>(prow, 2 * c + kg); });
-  {
-    const int grp = l >> 4, i = (l & 15) >> 2, r = l & 3;
-    static_for<D / 32>([&](auto dt) {
-      static_for<2>([&](auto hf) {
-        const int row = 8 * (grp >> 1) + 4 * hf + i;
-        const int chunk = 4 * dt + 2 * (grp & 1) + (r & 1);
-        troff[dt][hf] = row * D + 8 * swt<S::KC>(row, chunk) + 4 * (r >> 1);
-      });
-    });
-  }
-  // staging: wave load u covers rows (w + 4u) * 64 / KC + l / KC of a tile
-  int kst[S::NK];
-  static_for<S::NK>([&](auto u) {
-    const int r = (w + kWaves * u) * (64 / S::KC) + l / S::KC;
-    kst[u] = r;
-  });
-
-  for (;;) {
-    if (tid == 0) s_item = take_item(hdr, kFwdQ, q_serve, q_left);
-    __syncthreads();
-    const int idx = __builtin_amdgcn_readfirstlane(s_item);
-    if (idx < 0) break;
-    const FwdItem it = items[idx];
-    const int64_t key0 = cu[it.sample];
-    const int head = it.head0 + (w % it.nh);
-    const int wrow0 = (w / it.nh) * kRows;
-    const int wrows = min(max(it.nrows - wrow0, 0), kRows);
-    const bool active = wrows > 0;
-    const int my_r = active ? min(ln, wrows - 1) : 0;
-    const int64_t row = (int64_t)it.q_row0 + wrow0 + my_r;
-    const int qloc = it.q_loc0 + wrow0 + my_r;
-    const int wave_qmin = it.q_loc0 + wrow0;
-    const int nkb = (it.q_loc0 + it.nrows - 1) / kFwdBN + 1;
-    const int wave_nkb = active ? (it.q_loc0 + wrow0 + wrows - 1) / kFwdBN + 1 : 0;
-
-    bf16x8 qf[D / 16], of[D / 16];
-    float l2 = 0.f, dd_q = 0.f;
-    if (active) {
-      const size_t off = ((size_t)row * h_q + head) * D + 8 * kg;
-#pragma unroll
-      for (int c = 0; c < D / 16; ++c) {
-        qf[c] = *reinterpret_cast<const bf16x8 *>(q + off + 16 * c);
-        of[c] = *reinterpret_cast<const bf16x8 *>(dout + off + 16 * c);
-      }
-      const float *st = stats + ((size_t)head * (nq_pad / kRows) + row / kRows) * 2 * kRows;
-      l2 = st[row % kRows];
-      dd_q = st[kRows + row % kRows];
-    }
-    wait_vm_known();
-    f32x16 acc[D / 32];
-    static_for<D / 32>([&](auto dt) { acc[dt] = mfma_zero(); });
-
-    // global -> LDS, asynchronous: K and V rows of key block b (keys past the
-    // buffer read the last key instead; they are masked)
-    auto issue = [&](int b, int sg) {
-      bf16 *Ks = smem + sg * S::STAGE;
-      bf16 *Vs = Ks + S::K_EL;
-      static_for<S::NK>([&](auto u) {
-        const int wl = w + kWaves * u;
-        const int r = kst[u];
-        int64_t key = key0 + (int64_t)b * kFwdBN + r;
-        key = key < n_kv ? key : n_kv - 1;
-        const size_t off = ((size_t)key * h_kv + it.g) * D + 8 * swt<S::KC>(r, l % S::KC);
-        g2l16(k + off, Ks + wl * 512);
-        g2l16(v + off, Vs + wl * 512);
-      });
-    };
-
-    // key blocks go in pairs: pair p = blocks 2p, 2p + 1 in stages 2 (p % 2)
-    // and 2 (p % 2) + 1; the loads of pair p + 1 overlap the compute of pair p
-    const int npairs = (nkb + 1) / 2;
-    auto issue_pair = [&](int p) {
-      issue(2 * p, 2 * (p & 1));
-      if (2 * p + 1 < nkb) issue(2 * p + 1, 2 * (p & 1) + 1);
-    };
-    issue_pair(0);
-    for (int p = 0; p < npairs; ++p) {
-      wait_vm_n<0>();             // pair p, the only loads in flight
-      barrier_nofence();
-      // the stages of pair p - 1 are free again (every wave passed the barrier)
-      if (p + 1 < npairs) issue_pair(p + 1);
-      for (int b = 2 * p; b < 2 * p + 2 && b < nkb; ++b) {
-      if (b < wave_nkb) {
-        const bf16 *Ks = smem + (2 * (p & 1) + (b & 1)) * S::STAGE;
-        const bf16 *Vs = Ks + S::K_EL;
-        f32x16 s[2], dp[2];
-        static_for<2>([&](auto t) {
-          static_for<16>([&](auto r) { s[t][int(r)] = 0.f; dp[t][int(r)] = 0.f; });
-          static_for<D / 16>([&](auto c) {
-            s[t] = mfma32(*reinterpret_cast<const bf16x8 *>(Ks + 32 * t * D + koff[c]), qf[c],
-                          s[t]);
-            dp[t] = mfma32(*reinterpret_cast<const bf16x8 *>(Vs + 32 * t * D + koff[c]), of[c],
-                           dp[t]);
-          });
-        });
-        sched_pipeline<4 * (D / 16), 4>();
-        // causal mask only in blocks that reach past the wave's first row
-        if (b * kFwdBN + kFwdBN - 1 > wave_qmin) {
-          static_for<2>([&](auto t) {
-            static_for<16>([&](auto r) {
-              const int kl = b * kFwdBN + 32 * t + 16 * (r >> 3) + 8 * kg + (r & 7);
-              if (kl > qloc) s[t][int(r)] = -INFINITY;
-            });
-          });
-        }
-        bf16x8 dsf[4];
-        const float neg_l2 = -l2;
-        static_for<2>([&](auto t) {
-          static_for<16>([&](auto r) {
-            const float p = fast_exp2(__builtin_fmaf(s[t][int(r)], c2, neg_l2));
-            dsf[2 * t + (r >> 3)][r & 7] = static_cast<bf16>(p * (dp[t][int(r)] - dd_q));
-          });
-        });
-        // dQ^T += K^T dS^T; key chunk c = 16 keys from tile row 16 c
-        static_for<D / 32>([&](auto dt) {
-          static_for<4>([&](auto c) {
-            const bf16 *base = Ks + 16 * c * D;
-            acc[dt] = mfma32(lds_tr16x2(base + troff[dt][0], base + troff[dt][1]), dsf[c],
-                             acc[dt]);
-          });
-        });
-        sched_pipeline<4 * (D / 32), 4>();
-      }
-      }
-    }
-    wait_vm_n<0>();
-    __syncthreads();   // the ring is reused by the next item
-
-    if (active && ln < wrows) {
-      bf16 *op = dq + ((size_t)row * h_q + head) * D + 8 * kg;
-#pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt)
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          bf16x8 ov;
-#pragma unroll
-          for (int i = 0; i < 8; ++i) ov[i] = static_cast<bf16>(acc[dt][8 * hh + i] * scale);
-          *reinterpret_cast<bf16x8 *>(op + 32 * dt + 16 * hh) = ov;
-        }
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
 static size_t align256b(size_t x) { return (x + 255) / 256 * 256; }
 
 BwdLayout bwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, int h_kv, int d) {
@@ -794,10 +588,7 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
   if (!attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_bwd_dkdv_kernel<D>),
                             hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)KvShape<D>::SMEM) != hipSuccess ||
-        hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_bwd_dq_kernel<D>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)DqShape<D>::SMEM) != hipSuccess)
+                            (int)KvShape<D>::SMEM) != hipSuccess)
       return fail(LIBRA_EHIP, "hipFuncSetAttribute failed");
     attr_set = true;
   }
@@ -828,11 +619,9 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
                        v, q, dout, aug, cu, tiles, T, items, hdr, h_q, h_kv, n_q, n_kv,
                        L.nq_pad, scale, scale * kLog2e, dk, dv, accumulate ? 1 : 0);
     if (tm_kv) hipEventRecord(tm_kv->end, st);
-    if (tm_q) hipEventRecord(tm_q->begin, st);
-    hipLaunchKernelGGL(attn_bwd_dq_kernel<D>, dim3(cus), dim3(kThreads), DqShape<D>::SMEM, st, q,
-                       dout, k, v, stats, cu, qitems, hdr, h_q, h_kv, n_q, n_kv, L.nq_pad,
-                       scale * kLog2e, scale, dq);
-    if (tm_q) hipEventRecord(tm_q->end, st);
+    const int rc = launch_bwd_dq(D, q, dout, k, v, stats, cu, qitems, hdr, h_q, h_kv, n_q, n_kv,
+                                 L.nq_pad, scale, dq, cus, st, tm_q);
+    if (rc != LIBRA_OK) return rc;
   }
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(LIBRA_EHIP, "backward launch failed: %s", hipGetErrorString(e));

@@ -149,6 +149,7 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+
 // Swizzle of row-major Q / dO / K / V tiles that are read both by rows
 // (16-byte reads, 16 consecutive rows per pass) and by the LDS transpose
 // reads below (8-byte reads of 4 rows x 64 bytes per pass, rows 4j..4j+3).
@@ -272,6 +273,7 @@ __device__ __forceinline__ void g2l16x2(const void *ga, const void *gb, uint32_t
 // they publish complete first (s_waitcnt on the loads that filled it).
 __device__ __forceinline__ void barrier_nofence() { __builtin_amdgcn_s_barrier(); }
 
+
 // s_waitcnt vmcnt(0) that the compiler's wait-count pass sees (unlike an
 // inline-asm wait): after it, registers loaded from global memory count as
 // ready, so no wait for them is placed inside a loop that follows, where it
@@ -308,6 +310,51 @@ __device__ __forceinline__ void static_for_impl(F &&f) {
 template <int N, typename F>
 __device__ __forceinline__ void static_for(F &&f) {
   static_for_impl<0, N>(f);
+}
+
+// As sched_pipeline, with R DS reads per MFMA: AHEAD reads first, then per
+// MFMA one MFMA and the next R reads while any remain.
+template <int N, int R, int AHEAD>
+__device__ __forceinline__ void sched_pipeline_r() {
+  __builtin_amdgcn_sched_group_barrier(0x100, AHEAD, 0);
+  static_for<N>([&](auto i) {
+    constexpr int left = N * R - AHEAD - int(i) * R;
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, left >= R ? R : (left > 0 ? left : 0), 0);
+  });
+}
+
+// x as hi + mid + lo, three bf16 values in elements 0..2 of r, the rest zero
+// (exact to about 2^-24 |x|).  Against a k-block of ones in k = 0, 1, 2 an
+// MFMA adds x itself to every accumulator of the row (or column).
+__device__ __forceinline__ void split3(float x, bf16x8 &r) {
+  const bf16 a = static_cast<bf16>(x);
+  const float x1 = x - static_cast<float>(a);
+  const bf16 b = static_cast<bf16>(x1);
+  const bf16 c = static_cast<bf16>(x1 - static_cast<float>(b));
+  static_for<8>([&](auto i) { r[int(i)] = bf16(0.f); });
+  r[0] = a;
+  r[1] = b;
+  r[2] = c;
+}
+
+// s_waitcnt vmcnt(N) for a compile-time N.
+template <int N>
+__device__ __forceinline__ void wait_vm_n() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+// Wait until at most k * L vector-memory operations are outstanding
+// (k in [0, KMAX]; larger k wait for KMAX * L).
+template <int L, int KMAX>
+__device__ __forceinline__ void wait_stages(int k) {
+  bool done = false;
+  static_for<KMAX>([&](auto i) {
+    if (!done && k == int(i)) {
+      wait_vm_n<int(i) * L>();
+      done = true;
+    }
+  });
+  if (!done) wait_vm_n<KMAX * L>();
 }
 
 // A zero accumulator produced by an MFMA: in kernels whose MFMAs write
@@ -378,6 +425,12 @@ int launch_fwd(const void *q, const void *k, const void *v, const int64_t *cu, i
                const libra_tile_t *tiles, int64_t T, int64_t n_q, int64_t n_kv, int h_q,
                int h_kv, int d, float scale, void *o, float *lse, void *ws,
                const FwdLayout &L, hipStream_t st, const KernelTimer *tm);
+// The dQ kernel of the backward pass (attn_bwd_dq.hip), on `blocks`
+// persistent workgroups over the forward-style work items.
+int launch_bwd_dq(int d, const bf16 *q, const bf16 *dout, const bf16 *k, const bf16 *v,
+                  const float *stats, const int64_t *cu, const FwdItem *items, int32_t *hdr,
+                  int h_q, int h_kv, int64_t n_q, int64_t n_kv, int64_t nq_pad, float scale,
+                  bf16 *dq, int blocks, hipStream_t st, const KernelTimer *tm);
 int launch_bwd(const void *q, const void *k, const void *v, const void *o, const float *lse,
                const void *dout, const int64_t *cu, int64_t n, const libra_tile_t *tiles,
                int64_t T, int64_t n_q, int64_t n_kv, int h_q, int h_kv, int d, float scale,
