@@ -6,24 +6,24 @@
 // dS = P * (dO V^T - D), dQ = scale dS K, dK = scale dS^T Q.
 //
 // Two persistent kernels, no atomics (every output element has one writer):
-//   * dK / dV, KV-stationary: a work item is 128 keys of one KV head of one
-//     sample (anchored at the sample start); each of the 4 waves keeps 32 keys
-//     of K and V in registers plus fp32 dK^T / dV^T accumulators and loops
-//     over the 32-row query blocks of the tiles that attend them and over the
-//     query heads of the KV group.  S and dP are computed with queries on M
-//     (lane = key), exactly the operand layout that dV^T = dO^T P and
-//     dK^T = Q^T dS need; the dO^T / Q^T operands come from the same
-//     row-major LDS tiles through the LDS transpose reads.  Query blocks are
-//     staged in an LDS ring, up to seven ahead of the one computed.
-//   * dQ (attn_bwd_dq.hip), query-stationary, shaped like the forward: S^T = K Q^T and
-//     dP^T = V dO^T (lane = query), dS^T = P^T * (dP^T - D), then
-//     dQ^T += K^T dS^T; key blocks are staged in a 4-deep LDS ring.  It recomputes S and dP instead of accumulating dQ
-//     across key blocks with atomics: on long samples that accumulation is
-//     read-modify-write traffic of 4 bytes x d per (32 queries x 128 keys)
-//     per head, which would bound the whole backward by HBM.
-// Preparation: D = rowsum(dO * O) and the two work-item lists, longest
-// first.  Every transposed operand (dO^T, Q^T, K^T) is read from row-major
-// LDS tiles with the LDS transpose reads.
+//   * dK / dV (here), KV-stationary: a work item is 128 keys of one KV head of
+//     one sample (anchored at the sample start); each of the 4 waves keeps 32
+//     keys of K and V in registers plus fp32 dK^T / dV^T accumulators and
+//     loops over the 32-row query blocks of the tiles that attend them, two
+//     query heads of the KV group per step.  S and dP are computed with
+//     queries on M (lane = key), exactly the operand layout that dV^T = dO^T P
+//     and dK^T = Q^T dS need; the dO^T / Q^T operands come from the same
+//     row-major LDS tiles through the LDS transpose reads.  LSE and D enter
+//     the S and dP products as one extra k-block (see bwd_pre_kernel), so the
+//     VALU only exponentiates and multiplies.  Steps are staged in a 4-deep
+//     LDS ring, two ahead of the one computed.
+//   * dQ (attn_bwd_dq.hip), query-stationary, shaped like the forward.  It
+//     recomputes S and dP instead of accumulating dQ across key blocks with
+//     atomics: on long samples that accumulation is read-modify-write traffic
+//     of 4 bytes x d per (32 queries x 128 keys) per head, which would bound
+//     the whole backward by HBM.
+// Preparation: D = rowsum(dO * O), the augmented operands and the two
+// work-item lists, longest first.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
