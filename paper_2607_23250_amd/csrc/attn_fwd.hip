@@ -127,6 +127,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
       });
     });
   }
+  // staging: wave load u covers rows (w + 4u) * 64 / KC + l / KC of a tile;
+  // k_lane[u] is the lane's byte offset from the block's first K (V) row
+  static_assert(S::NK % 2 == 0, "staging copies go four at a time");
+  uint32_t k_lane[S::NK];
+  static_for<S::NK>([&](auto u) {
+    const int r = (w + kWaves * u) * (64 / S::KC) + l / S::KC;
+    k_lane[u] = 2u * (uint32_t)(r * h_kv * D + 8 * swt<S::KC>(r, l % S::KC));
+  });
 
   for (;;) {
     if (tid == 0) s_item = take_item(hdr, kFwdQ, q_serve, q_left);
@@ -161,6 +169,19 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     auto issue = [&](int b, int buf) {
       bf16 *Ks = smem + buf * S::STAGE;
       bf16 *Vs = Ks + S::K_EL;
+      const int64_t kb0 = key0 + (int64_t)b * kFwdBN;
+      if (kb0 + kFwdBN <= n_kv) {
+        // whole block inside the buffer: one SGPR base, fixed per-lane offsets
+        const size_t off = ((size_t)kb0 * h_kv + it.g) * D;
+        const uint32_t lk = lds_addr(Ks) + 1024u * w, lv = lds_addr(Vs) + 1024u * w;
+        static_for<S::NK / 2>([&](auto h) {
+          constexpr uint32_t d0 = 2 * h * kWaves * 1024u, d1 = d0 + kWaves * 1024u;
+          g2l16x4(k + off, v + off, k_lane[2 * h], k_lane[2 * h + 1], lk + d0, lk + d1, lv + d0,
+                  lv + d1);
+        });
+        return;
+      }
+      // the last block of the buffer: keys past it read the last key (masked)
       static_for<S::NK>([&](auto u) {
         const int wl = w + kWaves * u;
         const int r = wl * (64 / S::KC) + l / S::KC;
