@@ -332,16 +332,20 @@ def launch_sets(w, full_tiles, share_tiles):
 def traffic_entry(kernel: str, workload: str):
     """HBM bytes per launch from the committed rocprofv3 PMC summary of this
     kernel on this workload, or None when missing or taken on a different
-    kernel source."""
+    kernel source (sha256 over the listed source files, in order)."""
     path = os.path.join(ROOT, "profiles", f"{kernel}__{workload}__traffic.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    src = os.path.join(ROOT, "paper_2607_23250_amd", "csrc", rec.get("source", ""))
-    if not os.path.exists(src):
-        return None
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
-    if sha != rec.get("source_sha256"):
+    srcs = rec.get("source", [])
+    srcs = [srcs] if isinstance(srcs, str) else srcs
+    h = hashlib.sha256()
+    for name in srcs:
+        src = os.path.join(ROOT, "paper_2607_23250_amd", "csrc", name)
+        if not os.path.exists(src):
+            return None
+        h.update(open(src, "rb").read())
+    if not srcs or h.hexdigest() != rec.get("source_sha256"):
         return None
     return rec.get("bytes_per_launch")
 
@@ -357,9 +361,15 @@ def cpu_baseline(w, q, k, v, do, seconds):
     done_rows = []
     t0 = time.perf_counter()
     i = 0
-    while time.perf_counter() - t0 < seconds and i < len(order):
-        rows = np.sort(order[i:i + 2])
-        i += 2
+    # one row at a time; stop before a row that, at the mean time per row so
+    # far, would end past the budget (rows differ a lot: a row attends its
+    # sample's preceding keys, up to the whole 900K-token sample)
+    while i < len(order):
+        el = time.perf_counter() - t0
+        if done_rows and el + el / len(done_rows) > seconds:
+            break
+        rows = order[i:i + 1]
+        i += 1
         oa.attention_fwd(q, k, v, w.lengths, pos, rows=rows)
         oa.attention_bwd(q, k, v, do, w.lengths, pos, rows=rows)
         done_rows.extend(rows.tolist())
