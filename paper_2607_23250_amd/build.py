@@ -30,17 +30,16 @@ def _hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-# Per-source extra flags.  The forward kernel takes its MFMA results in VGPRs
-# (two workgroups per CU; the default heuristic shuffles its accumulators
-# through AGPRs inside the hot loop).  The backward kernels keep their
-# long-lived dK / dV / dQ accumulators in AGPRs, the default form once they
-# are initialised by an MFMA, which leaves the 256 VGPRs to the operands in
-# flight (in VGPR form the dQ kernel runs out of registers for its LDS reads
-# and serialises them).
+# Per-source extra flags.  The forward and dK / dV kernels take the MFMA
+# results that the VALU reads (S, dP) in VGPRs; the default heuristic lands
+# them in AGPRs and copies every element out before use.  The compiler still
+# keeps the long-lived dK / dV accumulators in AGPRs.  The dQ kernel stays in
+# the default form: in VGPR form it runs out of registers for its LDS reads.
 _VGPR_FORM = ["-mllvm", "--amdgpu-mfma-vgpr-form=1"]
 EXTRA_FLAGS = {
     "attn_fwd.hip": _VGPR_FORM,
     "attn_api.hip": _VGPR_FORM,
+    "attn_bwd.hip": _VGPR_FORM,
 }
 
 
