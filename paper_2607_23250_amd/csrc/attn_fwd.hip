@@ -26,6 +26,22 @@
 
 namespace libra {
 
+// Lanes l and l ^ 32 hold the two halves of a query's row: v_permlane32_swap
+// on two copies of x pairs them up in every lane (lanes 0-31 get
+// (x[l], x[l + 32]), lanes 32-63 (x[l - 32], x[l])) without a round trip
+// through LDS; max and sum of the pair are symmetric, so both lanes of a row
+// get the same bits.
+__device__ __forceinline__ float row_max2(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float row_sum2(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // ---------------------------------------------------------------------------
 // Work items: every tile is split into sample fragments; every fragment into
 // items of (<= 4 heads of one KV group) x (32 * 4 / heads rows).
@@ -225,7 +241,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
         static_for<2>([&](auto t) {
           static_for<16>([&](auto r) { mx = fmaxf(mx, s[t][int(r)]); });
         });
-        mx = fmaxf(mx, __shfl_xor(mx, 32)) * c2;       // row max of the scaled scores (log2 units)
+        mx = row_max2(mx) * c2;       // row max of the scaled scores (log2 units)
         // Lazy rescaling: the running max only moves when the block max exceeds
         // it by more than 8 (a factor 256 in P).  The decision is per row, so
         // rows stay independent of each other; the wave skips the multiply
@@ -264,7 +280,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     }
 
     if (active) {
-      const float l_tot = l_run + __shfl_xor(l_run, 32);
+      const float l_tot = row_sum2(l_run);
       const float inv = 1.f / l_tot;
       if (ln < wrows) {
         bf16 *op = o + ((size_t)row * h_q + head) * D + 8 * kg;
