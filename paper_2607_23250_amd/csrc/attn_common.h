@@ -236,6 +236,31 @@ __device__ __forceinline__ void g2l16x4(const void *ga, const void *gb, uint32_t
       : "v"(o0), "v"(o1), "s"(la0), "s"(la1), "s"(lb0), "s"(lb1), "s"(ga), "s"(gb)
       : "memory");
 }
+// Four such copies from one base: rows at byte offsets o0 .. o3 from g land at
+// la0 .. la3.
+__device__ __forceinline__ void g2l16x4r(const void *g, uint32_t o0, uint32_t o1, uint32_t o2,
+                                         uint32_t o3, uint32_t la0, uint32_t la1, uint32_t la2,
+                                         uint32_t la3) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %5\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %9\n\t"
+      "s_mov_b32 m0, %6\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, %9\n\t"
+      "s_mov_b32 m0, %7\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %3, %9\n\t"
+      "s_mov_b32 m0, %8\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %4, %9\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(o0), "v"(o1), "v"(o2), "v"(o3), "s"(la0), "s"(la1), "s"(la2), "s"(la3), "s"(g)
+      : "memory");
+}
 // One such copy: lane bytes at byte offset o from the wave-uniform base g land
 // at LDS address la.
 __device__ __forceinline__ void g2l16s(const void *g, uint32_t o, uint32_t la) {

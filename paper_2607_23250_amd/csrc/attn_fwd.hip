@@ -145,7 +145,6 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
   }
   // staging: wave load u covers rows (w + 4u) * 64 / KC + l / KC of a tile;
   // k_lane[u] is the lane's byte offset from the block's first K (V) row
-  static_assert(S::NK % 2 == 0, "staging copies go four at a time");
   uint32_t k_lane[S::NK];
   static_for<S::NK>([&](auto u) {
     const int r = (w + kWaves * u) * (64 / S::KC) + l / S::KC;
@@ -179,21 +178,26 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     static_for<D / 32>([&](auto dt) { static_for<16>([&](auto r) { oacc[dt][int(r)] = 0.f; }); });
     float m_run = -INFINITY, l_run = 0.f;
 
-    // global -> LDS, asynchronous: K and V rows of key block b (keys past the
-    // buffer read the last key instead; keys past the row are masked, and
-    // their V rows meet P = 0)
-    auto issue = [&](int b, int buf) {
-      bf16 *Ks = smem + buf * S::STAGE;
-      bf16 *Vs = Ks + S::K_EL;
+    // global -> LDS, asynchronous: the K (part 0) or V (part 1) rows of key
+    // block b (keys past the buffer read the last key instead; keys past the
+    // row are masked, and their V rows meet P = 0)
+    auto issue = [&](int b, int buf, int part) {
+      const bf16 *src = part ? v : k;
+      bf16 *dst = smem + buf * S::STAGE + part * S::K_EL;
       const int64_t kb0 = key0 + (int64_t)b * kFwdBN;
       if (kb0 + kFwdBN <= n_kv) {
-        // whole block inside the buffer: one SGPR base, fixed per-lane offsets
-        const size_t off = ((size_t)kb0 * h_kv + it.g) * D;
-        const uint32_t lk = lds_addr(Ks) + 1024u * w, lv = lds_addr(Vs) + 1024u * w;
-        static_for<S::NK / 2>([&](auto h) {
-          constexpr uint32_t d0 = 2 * h * kWaves * 1024u, d1 = d0 + kWaves * 1024u;
-          g2l16x4(k + off, v + off, k_lane[2 * h], k_lane[2 * h + 1], lk + d0, lk + d1, lv + d0,
-                  lv + d1);
+        // whole block inside the buffer: one SGPR base, fixed per-lane offsets;
+        // wave load u lands 1 KiB x (w + kWaves u) into the tile
+        const bf16 *base = src + ((size_t)kb0 * h_kv + it.g) * D;
+        const uint32_t ld = lds_addr(dst) + 1024u * w;
+        static_for<S::NK / 4>([&](auto h) {
+          constexpr uint32_t d = 4 * h * kWaves * 1024u, e = kWaves * 1024u;
+          g2l16x4r(base, k_lane[4 * h], k_lane[4 * h + 1], k_lane[4 * h + 2], k_lane[4 * h + 3],
+                   ld + d, ld + d + e, ld + d + 2 * e, ld + d + 3 * e);
+        });
+        static_for<S::NK % 4>([&](auto i) {
+          constexpr int u = S::NK / 4 * 4 + i;
+          g2l16s(base, k_lane[u], ld + u * kWaves * 1024u);
         });
         return;
       }
@@ -204,18 +208,22 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
         const int col = swt<S::KC>(r, l % S::KC);
         int64_t key = key0 + (int64_t)b * kFwdBN + r;
         key = key < n_kv ? key : n_kv - 1;
-        const size_t off = ((size_t)key * h_kv + it.g) * D + 8 * col;
-        g2l16(k + off, Ks + wl * 512);
-        g2l16(v + off, Vs + wl * 512);
+        g2l16(src + ((size_t)key * h_kv + it.g) * D + 8 * col, dst + wl * 512);
       });
     };
 
-    issue(0, 0);
+    issue(0, 0, 0);
+    issue(0, 0, 1);
     wait_vm();
     __syncthreads();
     for (int b = 0; b < nkb; ++b) {
       const int buf = b & 1;
-      if (b + 1 < nkb) issue(b + 1, buf ^ 1);
+      // the next block's K rows now, its V rows after this block's S^T
+      // products (the other workgroup on the CU keeps the matrix cores busy
+      // while this one waits to issue)
+      const bool more = b + 1 < nkb;
+      if (more) issue(b + 1, buf ^ 1, 0);
+      if (b >= wave_nkb && more) issue(b + 1, buf ^ 1, 1);
       if (b < wave_nkb) {
         const bf16 *Ks = smem + buf * S::STAGE;
         const bf16 *Vs = Ks + S::K_EL;
@@ -227,6 +235,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
             s[t] = mfma32(*reinterpret_cast<const bf16x8 *>(kp + koff[c]), qf[c], s[t]);
           });
         });
+        if (more) issue(b + 1, buf ^ 1, 1);
         // keys past the row are masked only in blocks that reach past the
         // wave's first row (the diagonal block of each row)
         if (b * kFwdBN + kFwdBN - 1 > wave_qmin) {
