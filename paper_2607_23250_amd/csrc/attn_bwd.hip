@@ -81,17 +81,48 @@ __global__ __launch_bounds__(kPrepThreads) void prep_bwd_kernel(
   }
   __threadfence();
   __syncthreads();
+  // Samples with more than kCoopBlocks key blocks are enumerated by the
+  // whole workgroup (key blocks across the threads), the others by one
+  // thread each; if the list of long samples overflows, every sample goes the
+  // per-thread way.  Both enumerations below see the same items.
+  constexpr int kCoopBlocks = 64, kMaxLong = 256;
+  __shared__ int32_t longs[kMaxLong];
+  __shared__ int32_t n_long;
+  if (tid == 0) n_long = 0;
+  __syncthreads();
+  for (int64_t j = tid; j < n; j += kPrepThreads) {
+    const int32_t e = ld_agent(&ext[j]);
+    if ((e + kBwdBK - 1) / kBwdBK > kCoopBlocks) {
+      const int32_t slot = atomicAdd(&n_long, 1);
+      if (slot < kMaxLong) longs[slot] = (int32_t)j;
+    }
+  }
+  __syncthreads();
+  const bool coop = n_long <= kMaxLong;
+  auto emit = [&](auto &&f, int64_t j, int32_t e, int g, int kb) {
+    f(BwdItem{(int32_t)j, kb, g, 0}, (int64_t)(e - kb * kBwdBK + kRows - 1) / kRows,
+      (g * R + kb % R) % kXcds);
+  };
   auto each = [&](auto &&f) {
     for (int64_t j = tid; j < n; j += kPrepThreads) {
       const int32_t e = ld_agent(&ext[j]);
       if (e == 0) continue;
-      const unsigned long long mk = ld_agent(&gmask[j]);
       const int nkb = (e + kBwdBK - 1) / kBwdBK;
+      if (coop && nkb > kCoopBlocks) continue;
+      const unsigned long long mk = ld_agent(&gmask[j]);
       for (int g = 0; g < h_kv; ++g)
         if (mk >> g & 1ull)
-          for (int kb = 0; kb < nkb; ++kb)
-            f(BwdItem{(int32_t)j, kb, g, 0}, (int64_t)(e - kb * kBwdBK + kRows - 1) / kRows,
-              (g * R + kb % R) % kXcds);
+          for (int kb = 0; kb < nkb; ++kb) emit(f, j, e, g, kb);
+    }
+    if (!coop) return;
+    for (int i = 0; i < n_long; ++i) {
+      const int64_t j = longs[i];
+      const int32_t e = ld_agent(&ext[j]);
+      const int nkb = (e + kBwdBK - 1) / kBwdBK;
+      const unsigned long long mk = ld_agent(&gmask[j]);
+      for (int g = 0; g < h_kv; ++g)
+        if (mk >> g & 1ull)
+          for (int kb = tid; kb < nkb; kb += kPrepThreads) emit(f, j, e, g, kb);
     }
   };
   build_queues<BwdItem>(each, hist, part, hdr, kBwdQ, items, max_items);
