@@ -138,9 +138,25 @@ def test_full_size_sampled_rows(name):
 @pytest.mark.parametrize("name", wl.WORKLOADS[1:])
 def test_full_size_zero_k_closed_forms(name):
     w = wl.workload(name)
+    say(f"[full {name} K=0] rows={w.n_q_rows} keys={w.n_kv_rows}")
+    _check_zero_k(w, *_tensors(name))
+
+
+def test_many_long_samples_zero_k():
+    """More samples longer than 64 key blocks of 128 keys than the dK/dV item
+    builder lists for whole-workgroup enumeration (256): its per-thread path
+    then takes every sample; every output is checked against the K = 0 closed
+    forms."""
+    n_long, ell = 300, 8256                  # 65 key blocks each
+    w = wl.Workload("long300", 7, [[ell] * n_long], 2, 1, 64, B=8192, H=1, CP=1)
+    say(f"[many long samples K=0] samples={n_long} x {ell} rows={w.n_q_rows}")
+    _check_zero_k(w, *wl.tensors(w.seed, w.n_q_rows, w.n_kv_rows, w.h_q, w.h_kv, w.d))
+
+
+def _check_zero_k(w, q, kk, v, do):
+    """fwd + bwd with K = 0 in bench.py's launch configuration, every output
+    element against its closed form."""
     sets = _launch_sets(w)
-    say(f"[full {name} K=0] rows={w.n_q_rows} keys={w.n_kv_rows} launches={len(sets)}")
-    q, kk, v, do = _tensors(name)
     kk = torch.zeros_like(kk)
     o, lse, dq, dk, dv = _run(w, sets, q, kk, v, do, accumulate=True)
     pos = w.q_positions()
