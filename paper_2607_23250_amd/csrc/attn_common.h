@@ -337,18 +337,6 @@ __device__ __forceinline__ void static_for(F &&f) {
   static_for_impl<0, N>(f);
 }
 
-// As sched_pipeline, with R DS reads per MFMA: AHEAD reads first, then per
-// MFMA one MFMA and the next R reads while any remain.
-template <int N, int R, int AHEAD>
-__device__ __forceinline__ void sched_pipeline_r() {
-  __builtin_amdgcn_sched_group_barrier(0x100, AHEAD, 0);
-  static_for<N>([&](auto i) {
-    constexpr int left = N * R - AHEAD - int(i) * R;
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, left >= R ? R : (left > 0 ? left : 0), 0);
-  });
-}
-
 // x as hi + mid + lo, three bf16 values in elements 0..2 of r, the rest zero
 // (exact to about 2^-24 |x|).  Against a k-block of ones in k = 0, 1, 2 an
 // MFMA adds x itself to every accumulator of the row (or column).
