@@ -198,3 +198,64 @@ def test_bwd_per_worker_accumulate(seed):
     check("dQ", to_np(dq), dQ, bf16_out=True, ref_bf16=bq)
     check("dK", to_np(dk), dK, ref_bf16=bk)
     check("dV", to_np(dv), dV, ref_bf16=bv)
+
+
+def test_empty_tile_list():
+    """No tiles: the forward writes nothing, the backward writes nothing but
+    the zero dK / dV of bf16 mode (and adds nothing in accumulate mode)."""
+    w = wl.small_random(0)
+    say(f"[empty tiles] heads=({w.h_q},{w.h_kv}) d={w.d}")
+    q, k, v, do = _dev(*_inputs(w))
+    cu = cu_dev(w)
+    td = pl.tiles_to_device(np.zeros(0, dtype=pl.TILE_DTYPE), DEV)
+    o = torch.full_like(q, 7.0)
+    lse = torch.full((w.h_q, w.n_q_rows), 7.0, dtype=torch.float32, device=DEV)
+    pl.libra_attn_fwd(q, k, v, cu, td, o=o, lse=lse)
+    dq = torch.full_like(q, 7.0)
+    dk, dv = torch.full_like(k, 7.0), torch.full_like(v, 7.0)
+    pl.libra_attn_bwd(q, k, v, o, lse, do, cu, td, dq=dq, dk=dk, dv=dv)
+    dk32 = torch.full(k.shape, 7.0, dtype=torch.float32, device=DEV)
+    dv32 = torch.full_like(dk32, 7.0)
+    pl.libra_attn_bwd(q, k, v, o, lse, do, cu, td, dq=dq, dk=dk32, dv=dv32, accumulate=True)
+    torch.cuda.synchronize()
+    assert bool((o == 7.0).all()) and bool((lse == 7.0).all()) and bool((dq == 7.0).all())
+    assert torch.count_nonzero(dk).item() == 0 and torch.count_nonzero(dv).item() == 0
+    assert bool((dk32 == 7.0).all()) and bool((dv32 == 7.0).all())
+
+
+def test_out_of_range_tiles_are_skipped():
+    """Tiles outside the buffers are skipped on the device and counted in the
+    workspace header (int32 slot 4); the other tiles' results are bit-identical
+    to a call without them."""
+    w = wl.small_random(5)
+    say(f"[out-of-range tiles] heads=({w.h_q},{w.h_kv}) d={w.d} rows={w.n_q_rows}")
+    tiles, _ = plan(w)
+    bad = np.zeros(3, dtype=pl.TILE_DTYPE)
+    bad[0] = tiles[0]
+    bad[0]["q_end"] = w.n_kv_rows + 64                  # keys past the buffer
+    bad[1] = tiles[0]
+    bad[1]["head_end"] = w.h_q + 1                      # heads past the buffer
+    bad[2] = tiles[0]
+    bad[2]["q_row"] = w.n_q_rows                        # rows past the buffer
+    both = np.concatenate([tiles, bad])
+    q, k, v, do = _dev(*_inputs(w))
+    cu = cu_dev(w)
+    outs = []
+    for tl in (tiles, both):
+        td = pl.tiles_to_device(tl, DEV)
+        n = len(w.lengths)
+        wsf = pl.alloc_workspace(pl.libra_attn_workspace_size(len(tl), n, w.n_q_rows, w.n_kv_rows,
+                                                              w.h_q, w.h_kv, w.d, False), DEV)
+        wsb = pl.alloc_workspace(pl.libra_attn_workspace_size(len(tl), n, w.n_q_rows, w.n_kv_rows,
+                                                              w.h_q, w.h_kv, w.d, True), DEV)
+        o, lse = pl.libra_attn_fwd(q, k, v, cu, td, workspace=wsf)
+        dq, dk, dv = pl.libra_attn_bwd(q, k, v, o, lse, do, cu, td, workspace=wsb)
+        torch.cuda.synchronize()
+        skipped = (int(wsf[16:20].cpu().view(torch.int32).item()),
+                   int(wsb[16:20].cpu().view(torch.int32).item()))
+        outs.append(([to_np(x) for x in (o, lse, dq, dk, dv)], skipped))
+    (ref, skip0), (got, skip1) = outs
+    assert skip0 == (0, 0), skip0
+    assert skip1 == (3, 3), skip1
+    for name, a, b in zip(("O", "LSE", "dQ", "dK", "dV"), ref, got):
+        assert np.array_equal(a, b), f"{name} changed when out-of-range tiles were added"
