@@ -453,6 +453,8 @@ def main():
             h.numpy()[:] = np.ascontiguousarray(s).view(np.uint8)
 
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    # per launch set (virtual worker): events around its forward and its backward
+    ev_w = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in sets]
     split_ms = []
 
     def step(i, record):
@@ -466,13 +468,21 @@ def main():
             dv.zero_()
         if record:
             ev[0].record(stream)
-        for td in dev_tiles:
+        for j, td in enumerate(dev_tiles):
+            if record:
+                ev_w[j][0].record(stream)
             pl.libra_attn_fwd(qd, kd, vd, cud, td, o=o, lse=lse, workspace=ws)
+            if record:
+                ev_w[j][1].record(stream)
         if record:
             ev[1].record(stream)
-        for td in dev_tiles:
+        for j, td in enumerate(dev_tiles):
+            if record:
+                ev_w[j][2].record(stream)
             pl.libra_attn_bwd(qd, kd, vd, o, lse, dod, cud, td, dq=dq, dk=dk, dv=dv,
                               accumulate=acc, workspace=ws)
+            if record:
+                ev_w[j][3].record(stream)
         if record:
             ev[2].record(stream)
         make_plan((i + 1) % 2)          # host plans the next step while the GPU runs
@@ -485,6 +495,9 @@ def main():
     step(args.warmup, True)
     torch.cuda.synchronize()
     split_ms = (ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]))
+    # fwd + bwd time of each launch set: for a pool run per virtual worker,
+    # the one-GPU stand-in for each worker's share of the step
+    worker_ms = [e[0].elapsed_time(e[1]) + e[2].elapsed_time(e[3]) for e in ev_w]
 
     pl.libra_timing_enable(True)
     plan_ms.clear()
@@ -545,6 +558,8 @@ def main():
         "bwd_dq_kernel_useful_tflops": round(2.0 * w.d * cost / len(sets) / (dq_launch_ms * 1e-3)
                                              / 1e12, 1),
         "plan_ms": round(float(np.mean(plan_ms)), 3) if plan_ms else None,
+        "launch_set_ms": [round(x, 3) for x in worker_ms],
+        "launch_set_time_max_over_mean": round(max(worker_ms) / float(np.mean(worker_ms)), 4),
         "roofline": {
             "kernel": f"attn_bwd_dkdv_kernel<{w.d}>",
             "bound": "mfma",
