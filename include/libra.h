@@ -220,6 +220,30 @@ int libra_attn_bwd(const void *q, const void *k, const void *v, const void *o, c
 int libra_timing_enable(int enable);
 int libra_timing_read(int which, double *total_ms, int64_t *launches);
 
+/*
+ * Matrix-core reference loop (measurement aid): the bf16 MFMA throughput the
+ * device sustains under load, reported beside the published dense peak.
+ * libra_mfma_loop enqueues on `stream` one workgroup per compute unit, of
+ * 4 waves (waves_per_simd = 1) or 8 (= 2, two waves on every SIMD); each wave
+ * runs `iters` rounds of 4 independent v_mfma_f32_32x32x16_bf16 products
+ * (32768 flops each) and does no other work.
+ *   libra_mfma_loop_size: *record_words = uint64 words the record needs
+ *       (3 per workgroup), *products_per_iter = products per round over the
+ *       whole launch (flops of the launch = 32768 * iters * products_per_iter).
+ *   record: device buffer of >= record_words uint64, owned by the caller;
+ *       workgroup i writes record[3 i] = shader-clock cycles and
+ *       record[3 i + 1] = 100 MHz wall-clock ticks of wave 0's loop (their
+ *       ratio times 0.1 is the shader clock in GHz); record[3 i + 2] is not
+ *       written.
+ * The caller times the launch with events on the same stream.
+ * Errors: EINVAL (waves_per_simd not 1 or 2, iters < 1, NULL pointers),
+ * ENOSPC (record too small), EHIP.
+ */
+int libra_mfma_loop_size(int32_t waves_per_simd, int64_t *record_words,
+                         int64_t *products_per_iter);
+int libra_mfma_loop(int32_t waves_per_simd, int32_t iters, uint64_t *record,
+                    int64_t record_words, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

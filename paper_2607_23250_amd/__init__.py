@@ -33,7 +33,8 @@ assert TILE_DTYPE.itemsize == 56
 
 EXPORTED = ("libra_strerror", "libra_last_error", "libra_plan", "libra_vrsp",
             "libra_attn_workspace_size", "libra_attn_fwd", "libra_attn_bwd",
-            "libra_timing_enable", "libra_timing_read")
+            "libra_timing_enable", "libra_timing_read", "libra_mfma_loop_size",
+            "libra_mfma_loop")
 
 
 class LibraError(RuntimeError):
@@ -82,6 +83,11 @@ def lib() -> ctypes.CDLL:
     L.libra_timing_read.restype = ctypes.c_int
     L.libra_timing_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                     ctypes.POINTER(ctypes.c_int64)]
+    L.libra_mfma_loop_size.restype = ctypes.c_int
+    L.libra_mfma_loop_size.argtypes = [I32, ctypes.POINTER(ctypes.c_int64),
+                                       ctypes.POINTER(ctypes.c_int64)]
+    L.libra_mfma_loop.restype = ctypes.c_int
+    L.libra_mfma_loop.argtypes = [I32, I32, P, I64, P]
     _lib = L
     return L
 
@@ -175,6 +181,15 @@ def libra_timing_read(which: int) -> Tuple[float, int]:
     return ms.value, n.value
 
 
+def libra_mfma_loop_size(waves_per_simd: int) -> Tuple[int, int]:
+    """(uint64 words of the record, MFMA products per round over the launch)."""
+    words = ctypes.c_int64(0)
+    prods = ctypes.c_int64(0)
+    _check(lib().libra_mfma_loop_size(waves_per_simd, ctypes.byref(words), ctypes.byref(prods)),
+           "libra_mfma_loop_size")
+    return words.value, prods.value
+
+
 # ---------------------------------------------------------------------------
 # torch-facing helpers (device memory and streams only)
 
@@ -241,6 +256,17 @@ def libra_attn_fwd(q, k, v, cu_seqlens, tiles, *, softmax_scale: float = 0.0, o=
                                 o.data_ptr(), lse.data_ptr(), workspace.data_ptr(),
                                 workspace.numel(), _stream(q.device)), "libra_attn_fwd")
     return o, lse
+
+
+def libra_mfma_loop(waves_per_simd: int, iters: int, record) -> None:
+    """Enqueue the matrix-core reference loop on the current stream; ``record``
+    is a device int64 tensor of at least ``libra_mfma_loop_size(...)[0]``
+    words (per workgroup: shader cycles, 100 MHz ticks, unused)."""
+    torch = _torch()
+    if record.dtype != torch.int64 or not record.is_cuda or not record.is_contiguous():
+        raise ValueError("record: need a contiguous int64 device tensor")
+    _check(lib().libra_mfma_loop(waves_per_simd, iters, record.data_ptr(), record.numel(),
+                                 _stream(record.device)), "libra_mfma_loop")
 
 
 def libra_attn_bwd(q, k, v, o, lse, dout, cu_seqlens, tiles, *, softmax_scale: float = 0.0,

@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OUT_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "liblibra.so")
 
-HIP_SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "attn_bwd_dq.hip", "attn_api.hip"]
+HIP_SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "attn_bwd_dq.hip", "attn_api.hip", "mfma_loop.hip"]
 CXX_SOURCES = ["plan.cpp", "vrsp.cpp"]
 ARCH = os.environ.get("LIBRA_OFFLOAD_ARCH", "gfx950")
 
