@@ -59,6 +59,11 @@ def parse():
                     help="one-GPU straggler emulation on the 1M-token pack: fwd+bwd time of each "
                          "of the 16 zigzag CP rank shares vs each of the 16 Libra worker tile "
                          "sets (Algorithm 2), plus throughput per call vs block length x heads")
+    ap.add_argument("--straggler-pool", action="store_true",
+                    help="one-GPU straggler emulation on a VRSP pool of 8 packs of 262,144 "
+                         "tokens with CP=8 (64 workers): fwd+bwd time of a head-parallel "
+                         "(Ulysses) rank of every pack, of all 64 zigzag CP rank shares, and of "
+                         "all 64 Libra worker tile sets of the pool")
     ap.add_argument("--simulate", action="store_true",
                     help="offline planner simulation (host only): the LLN estimate of Eq. 3 "
                          "against production-order grouping, and TAP's (B, H) grid on "
@@ -257,6 +262,124 @@ def straggler_bench():
     print(json.dumps(out), flush=True)
 
 
+def straggler_pool_bench(pool_packs: int = 8, cp: int = 8, seed: int = 1, gbs: int = 64):
+    """The paper's core-attention straggler comparison (Sec. 6.3) on one GPU.
+
+    A window of `gbs` packed sequences of 262,144 tokens (the long-tailed 256K
+    stand-in) is grouped into pools of `pool_packs` by Algorithm 1; the pool
+    with the largest load (the one that sets the step) is run three ways, each
+    worker's share fwd+bwd alone on the GPU, best of two:
+      * head-parallel CP (Ulysses) per pack: a rank computes every row of its
+        pack for h_q / cp query heads, so the cp ranks of a pack are equal and
+        one is timed per pack;
+      * zigzag CP per pack: rank r computes its head and tail chunks, all heads;
+      * Libra: the whole pool planned by Algorithm 2 (B = 4096, H = 2) over
+        pool_packs * cp workers.
+    Every tile list comes from libra_plan; attention shapes are Qwen3-30B-A3B's
+    (32 query heads, 4 KV heads, d = 128)."""
+    import torch
+    import paper_2607_23250_amd as pl
+    import workloads as wl
+    dev = torch.device("cuda:0")
+    h_q, h_kv, d, B = 32, 4, 128, 4096
+    L = wl.VRSP_WINDOWS["256K"][0]
+    win = wl.vrsp_window("256K", gbs, seed)
+    order, pool_load, _ = pl.libra_vrsp(win, pool_packs)
+    k_top = int(np.argmax(pool_load))
+    packs = [win[int(j)] for j in order[k_top * pool_packs:(k_top + 1) * pool_packs]]
+    lengths = [x for p in packs for x in p]
+    cu = np.zeros(len(lengths) + 1, dtype=np.int64)
+    cu[1:] = np.cumsum(lengths)
+    n_all = len(packs) * L
+    g = torch.Generator(device=dev).manual_seed(12)
+
+    def rnd(shape):
+        return torch.randn(shape, device=dev, generator=g, dtype=torch.float32).to(torch.bfloat16)
+
+    q, k, v, do = rnd((n_all, h_q, d)), rnd((n_all, h_kv, d)), rnd((n_all, h_kv, d)), \
+        rnd((n_all, h_q, d))
+    o, dq = torch.empty_like(q), torch.empty_like(q)
+    lse = torch.empty((h_q, n_all), dtype=torch.float32, device=dev)
+    dk = torch.zeros((n_all, h_kv, d), dtype=torch.float32, device=dev)
+    dv = torch.zeros_like(dk)
+    cud = torch.from_numpy(cu).to(dev)
+    max_tiles = 4096
+    ws = pl.alloc_workspace(pl.libra_attn_workspace_size(max_tiles, len(lengths), n_all, n_all,
+                                                         h_q, h_kv, d, True), dev)
+
+    def plan_tiles(pack_lengths_, cp_, H, q_ranges=None, offset=0):
+        """Tiles of one pack, moved to its place in the pool; the buffers hold
+        every row of the pool, so a tile's row is its pool position."""
+        t, _ = pl.libra_plan(pack_lengths_, [L], block_tokens=B, head_shards=H, cp=cp_,
+                             num_q_heads=h_q, num_kv_heads=h_kv, head_dim=d, q_ranges=q_ranges)
+        t["q_begin"] += offset
+        t["q_end"] += offset
+        t["q_row"] = t["q_begin"]
+        return t
+
+    def run_set(tiles, reps=2):
+        assert 0 < len(tiles) <= max_tiles
+        td = pl.tiles_to_device(tiles, dev)
+        best = None
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            pl.libra_attn_fwd(q, k, v, cud, td, o=o, lse=lse, workspace=ws)
+            pl.libra_attn_bwd(q, k, v, o, lse, do, cud, td, dq=dq, dk=dk, dv=dv,
+                              accumulate=True, workspace=ws)
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t0) * 1e3
+            best = ms if best is None else min(best, ms)
+        return best, 14.0 * d * float(tiles["cost"].sum()) / 1e12
+
+    def summary(items):
+        ms = [x["ms"] for x in items]
+        return {"max_ms": round(max(ms), 2), "mean_ms": round(float(np.mean(ms)), 2),
+                "max_over_mean": round(max(ms) / float(np.mean(ms)), 4)}
+
+    uly, zig = [], []
+    for p, pk in enumerate(packs):
+        off = p * L
+        t = plan_tiles(pk, 1, cp, offset=off)           # head shards of width h_q / cp
+        ms, tf = run_set(t[t["head_begin"] == 0])
+        uly.append({"pack": p, "ms": round(ms, 2), "tflop": round(tf, 2)})
+        print(json.dumps({"ulysses_rank_of_pack": uly[-1]}), file=sys.stderr, flush=True)
+        for r in range(cp):
+            c = L // (2 * cp)
+            ranges = [(r * c, (r + 1) * c), ((2 * cp - 1 - r) * c, (2 * cp - r) * c)]
+            ms, tf = run_set(plan_tiles(pk, cp, 1, q_ranges=ranges, offset=off))
+            zig.append({"pack": p, "rank": r, "ms": round(ms, 2), "tflop": round(tf, 2)})
+        print(json.dumps({"zigzag_pack_done": p, "max_ms": max(x["ms"] for x in zig[-cp:])}),
+              file=sys.stderr, flush=True)
+    full, loads = pl.libra_plan(lengths, [L] * len(packs), block_tokens=B, head_shards=2, cp=cp,
+                                num_q_heads=h_q, num_kv_heads=h_kv, head_dim=d)
+    lib = []
+    for r in range(len(packs) * cp):
+        ms, tf = run_set(full[full["worker"] == r])
+        lib.append({"worker": r, "ms": round(ms, 2), "tflop": round(tf, 2)})
+    print(json.dumps({"libra_workers_done": len(lib)}), file=sys.stderr, flush=True)
+    su, sz, sl = summary(uly), summary(zig), summary(lib)
+    pack_work = [sum(x * x for x in pk) for pk in packs]
+    out = {"metric": "one-GPU straggler emulation, VRSP pool of 8 packs of 262,144 tokens, "
+                     "CP=8, 64 workers (fwd+bwd)",
+           "value": round(su["max_ms"] / sl["max_ms"], 3),
+           "unit": "x (head-parallel CP straggler / Libra straggler)",
+           "higher_is_better": True, "data": "synthetic",
+           "config": {"window": f"{gbs} packs of {L} tokens, 0.95 lognormal(644, 1.5) + "
+                                f"0.05 Pareto(1.1, 8192), seed {seed}",
+                      "pool": f"the heaviest of {len(pool_load)} Algorithm 1 pools of "
+                              f"{pool_packs}", "h_q": h_q, "h_kv": h_kv, "head_dim": d,
+                      "cp": cp, "block_tokens": B, "head_shards": 2},
+           "pack_sum_l2_max_over_mean": round(max(pack_work) / float(np.mean(pack_work)), 4),
+           "zigzag_straggler_over_libra": round(sz["max_ms"] / sl["max_ms"], 3),
+           "ulysses": dict(su, ranks_timed=uly),
+           "zigzag": dict(sz, ranks=zig),
+           "libra": dict(sl, plan_load_max_over_mean=round(float(len(loads) * loads.max()
+                                                                 / loads.sum()), 4),
+                         workers=lib)}
+    print(json.dumps(out), flush=True)
+
+
 def simulate():
     """Planner-only simulation on synthetic optimizer-step windows."""
     import math
@@ -431,6 +554,9 @@ def main():
         return
     if args.straggler:
         straggler_bench()
+        return
+    if args.straggler_pool:
+        straggler_pool_bench()
         return
     if args.simulate:
         simulate()
