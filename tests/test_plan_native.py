@@ -122,3 +122,56 @@ def test_error_paths():
     # costs beyond int64: one sample of 2^32 tokens with 2^31 heads per shard
     _expect(pl.LIBRA_EOVERFLOW, lengths=[1 << 32], pack_tokens=[1 << 32], block_tokens=1 << 30,
             head_shards=1, cp=1, num_q_heads=1 << 30, num_kv_heads=1, head_dim=64)
+
+
+def _vrsp_pool(kind="256K", gbs=64, seed=1, P=8):
+    """The heaviest Algorithm 1 pool of a synthetic window (the pool of the
+    straggler emulation): its packs' sample lengths."""
+    win = wl.vrsp_window(kind, gbs, seed)
+    order, pool_load, _ = pl.libra_vrsp(win, P)
+    k = int(np.argmax(pool_load))
+    return [win[int(j)] for j in order[k * P:(k + 1) * P]]
+
+
+def test_pool_of_eight_256k_packs_cp8_bit_exact():
+    """64 workers (P = 8 packs of 262,144 tokens, CP = 8), B = 4096, H = 2:
+    the largest placement the benchmarks run, bit-exact against the oracle."""
+    packs = _vrsp_pool()
+    L = 262144
+    w = wl.Workload("pool8x256K-cp8", 0, packs, 32, 4, 128, B=4096, H=2, CP=8)
+    assert w.pack_tokens == [L] * 8 and w.V == 64
+    native, oracle = _native(w), _oracle(w)
+    _same(native, oracle)
+    assert w.V * native[1].max() / native[1].sum() <= 1.05
+
+
+def test_pool_splits_partition_the_work():
+    """The three splits of the pool straggler emulation: a head-parallel rank
+    (h_q / CP heads, every row of its pack) times CP, the 2 CP zigzag shares
+    of every pack, and Algorithm 2's workers each carry exactly the pool's
+    h_q * sum l(l+1)/2 causal pairs, and each zigzag rank's rows are its head
+    and tail chunks."""
+    packs = _vrsp_pool()
+    L, cp, h_q = 262144, 8, 32
+    exact = h_q * sum(x * (x + 1) // 2 for p in packs for x in p)
+    kw = dict(block_tokens=4096, num_q_heads=h_q, num_kv_heads=4, head_dim=128)
+    uly = zig = 0
+    for p in packs:
+        t, _ = pl.libra_plan(p, [L], head_shards=cp, cp=1, **kw)
+        first = t[t["head_begin"] == 0]
+        assert (first["head_end"] == h_q // cp).all()
+        assert first["q_begin"].min() == 0 and first["q_end"].max() == L
+        uly += int(first["cost"].sum()) * cp
+        c = L // (2 * cp)
+        for r in range(cp):
+            ranges = [(r * c, (r + 1) * c), ((2 * cp - 1 - r) * c, (2 * cp - r) * c)]
+            tz, _ = pl.libra_plan(p, [L], head_shards=1, cp=cp, q_ranges=ranges, **kw)
+            rows = np.concatenate([np.arange(a, b) for a, b in zip(tz["q_begin"], tz["q_end"])])
+            want = np.concatenate([np.arange(a, b) for a, b in ranges])
+            assert np.array_equal(np.sort(rows), want)
+            zig += int(tz["cost"].sum())
+    lengths = [x for p in packs for x in p]
+    full, loads = pl.libra_plan(lengths, [L] * len(packs), head_shards=2, cp=cp, **kw)
+    assert uly == exact and zig == exact
+    assert int(full["cost"].sum()) == exact == int(loads.sum())
+    assert sorted(set(full["worker"].tolist())) == list(range(len(packs) * cp))
