@@ -44,23 +44,31 @@ __device__ __forceinline__ float row_sum2(float x) {
 
 // ---------------------------------------------------------------------------
 // Work items: every tile is split into sample fragments; every fragment into
-// items of (<= 4 heads of one KV group) x (32 * 4 / heads rows).
+// items of (<= 4 heads of one KV group) x (32 * 4 / heads rows), starting at
+// the fragment's first row.  The enumeration goes by 32-row windows of a tile:
+// f(item, key blocks) is called for the items whose first row lies in rows
+// [wa, wb) of tile t (wb - wa <= 32, so at most one item per fragment and
+// head chunk), which spreads a tile's items over many threads.
 template <typename F>
-__device__ void for_each_fwd_item(const libra_tile_t &t, const int64_t *cu, int64_t n, int G,
-                                  F &&f) {
-  int64_t j = upper_bound64(cu, n, t.q_begin) - 1;
-  for (; j < n && cu[j] < t.q_end; ++j) {
+__device__ void for_each_fwd_item_in(const libra_tile_t &t, int64_t wa, int64_t wb,
+                                     const int64_t *cu, int64_t n, int G, F &&f) {
+  int64_t j = upper_bound64(cu, n, wa) - 1;
+  for (; j < n && cu[j] < wb; ++j) {
     const int64_t pb = t.q_begin > cu[j] ? t.q_begin : cu[j];
     const int64_t pe = t.q_end < cu[j + 1] ? t.q_end : cu[j + 1];
     const int32_t row0 = (int32_t)(t.q_row + (pb - t.q_begin));
     const int32_t qloc0 = (int32_t)(pb - cu[j]);
     const int32_t nfrag = (int32_t)(pe - pb);
+    const int64_t lim = wb < pe ? wb : pe;
     for (int g = t.head_begin / G; g * G < t.head_end; ++g) {
       const int hl = max(t.head_begin, g * G), hh = min(t.head_end, (g + 1) * G);
       for (int h0 = hl; h0 < hh; h0 += 4) {
         const int nh = min(4, hh - h0);
         const int rows_per = kRows * (4 / nh);
-        for (int rb = 0; rb < nfrag; rb += rows_per) {
+        // first item start pb + k rows_per at or after wa
+        int64_t k = wa > pb ? (wa - pb + rows_per - 1) / rows_per : 0;
+        for (; pb + k * rows_per < lim; ++k) {
+          const int32_t rb = (int32_t)(k * rows_per);
           const int nrows = min(rows_per, nfrag - rb);
           FwdItem it{row0 + rb, qloc0 + rb, (int32_t)j, h0, nh, nrows, g, 0};
           f(it, (qloc0 + rb + nrows - 1) / kFwdBN + 1);
@@ -79,23 +87,43 @@ __global__ __launch_bounds__(kPrepThreads) void prep_fwd_kernel(
     FwdItem *__restrict__ items, int64_t max_items) {
   __shared__ int32_t hist[kXcds * kQBuckets];
   __shared__ int32_t part[kPrepThreads];
+  __shared__ unsigned long long s_wmax;
   const int tid = threadIdx.x;
   const int G = h_q / h_kv;
   const int chunks = (G + 3) / 4;                    // head chunks per KV group
   const int keys = h_kv * chunks;
   const int R = keys >= kXcds ? 1 : kXcds / keys;    // queues per key
-  if (tid == 0) hdr[kBadTiles] = 0;
+  if (tid == 0) {
+    hdr[kBadTiles] = 0;
+    s_wmax = 0;
+  }
   __threadfence();
   __syncthreads();
+  // bad tiles, and the 32-row windows of the longest good tile
   int bad = 0;
-  for (int64_t t = tid; t < T; t += kPrepThreads)
-    if (!tile_ok(tiles[t], n_q, n_kv, h_q)) ++bad;
+  unsigned long long wm = 0;
+  for (int64_t t = tid; t < T; t += kPrepThreads) {
+    const libra_tile_t tl = tiles[t];
+    if (!tile_ok(tl, n_q, n_kv, h_q)) {
+      ++bad;
+      continue;
+    }
+    const unsigned long long w = (unsigned long long)((tl.q_end - tl.q_begin + kRows - 1) / kRows);
+    wm = w > wm ? w : wm;
+  }
   if (bad) atomicAdd(&hdr[kBadTiles], bad);
+  if (wm) atomicMax(&s_wmax, wm);
+  __syncthreads();
+  const int64_t wmax = (int64_t)s_wmax;
   auto each = [&](auto &&f) {
-    for (int64_t t = tid; t < T; t += kPrepThreads) {
+    for (int64_t v = tid; v < T * wmax; v += kPrepThreads) {
+      const int64_t t = v / wmax, w = v % wmax;
       const libra_tile_t tl = tiles[t];
       if (!tile_ok(tl, n_q, n_kv, h_q)) continue;
-      for_each_fwd_item(tl, cu, n, G, [&](const FwdItem &it, int nkb) {
+      const int64_t wa = tl.q_begin + (int64_t)kRows * w;
+      if (wa >= tl.q_end) continue;
+      const int64_t wb = wa + kRows < tl.q_end ? wa + kRows : tl.q_end;
+      for_each_fwd_item_in(tl, wa, wb, cu, n, G, [&](const FwdItem &it, int nkb) {
         const int key = it.g * chunks + (it.head0 - it.g * G) / 4;
         const int x = (key * R + (it.q_row0 / 128) % R) % kXcds;
         f(it, (int64_t)nkb, x);
