@@ -59,11 +59,12 @@ def parse():
                     help="one-GPU straggler emulation on the 1M-token pack: fwd+bwd time of each "
                          "of the 16 zigzag CP rank shares vs each of the 16 Libra worker tile "
                          "sets (Algorithm 2), plus throughput per call vs block length x heads")
-    ap.add_argument("--straggler-pool", action="store_true",
-                    help="one-GPU straggler emulation on a VRSP pool of 8 packs of 262,144 "
-                         "tokens with CP=8 (64 workers): fwd+bwd time of a head-parallel "
-                         "(Ulysses) rank of every pack, of all 64 zigzag CP rank shares, and of "
-                         "all 64 Libra worker tile sets of the pool")
+    ap.add_argument("--straggler-pool", nargs="?", const="256K", choices=("256K", "1M"),
+                    help="one-GPU straggler emulation on the heaviest VRSP pool of a synthetic "
+                         "window: 256K = 8 packs of 262,144 tokens with CP=8, 1M = 4 packs of "
+                         "1,048,576 tokens with CP=16 (64 workers either way); fwd+bwd time of "
+                         "a head-parallel (Ulysses) rank of every pack, of all zigzag CP rank "
+                         "shares, and of all Libra worker tile sets of the pool"),
     ap.add_argument("--simulate", action="store_true",
                     help="offline planner simulation (host only): the LLN estimate of Eq. 3 "
                          "against production-order grouping, and TAP's (B, H) grid on "
@@ -262,18 +263,19 @@ def straggler_bench():
     print(json.dumps(out), flush=True)
 
 
-def straggler_pool_bench(pool_packs: int = 8, cp: int = 8, seed: int = 1, gbs: int = 64):
+def straggler_pool_bench(kind: str = "256K", pool_packs: int = 8, cp: int = 8, seed: int = 1,
+                         gbs: int = 64, B: int = 4096, reps: int = 2):
     """The paper's core-attention straggler comparison (Sec. 6.3) on one GPU.
 
-    A window of `gbs` packed sequences of 262,144 tokens (the long-tailed 256K
-    stand-in) is grouped into pools of `pool_packs` by Algorithm 1; the pool
-    with the largest load (the one that sets the step) is run three ways, each
-    worker's share fwd+bwd alone on the GPU, best of two:
+    A window of `gbs` packed sequences (the long-tailed 256K or 1M stand-in)
+    is grouped into pools of `pool_packs` by Algorithm 1; the pool with the
+    largest load (the one that sets the step) is run three ways, each worker's
+    share fwd+bwd alone on the GPU, best of `reps`:
       * head-parallel CP (Ulysses) per pack: a rank computes every row of its
         pack for h_q / cp query heads, so the cp ranks of a pack are equal and
         one is timed per pack;
       * zigzag CP per pack: rank r computes its head and tail chunks, all heads;
-      * Libra: the whole pool planned by Algorithm 2 (B = 4096, H = 2) over
+      * Libra: the whole pool planned by Algorithm 2 (block B, H = 2) over
         pool_packs * cp workers.
     Every tile list comes from libra_plan; attention shapes are Qwen3-30B-A3B's
     (32 query heads, 4 KV heads, d = 128)."""
@@ -281,9 +283,9 @@ def straggler_pool_bench(pool_packs: int = 8, cp: int = 8, seed: int = 1, gbs: i
     import paper_2607_23250_amd as pl
     import workloads as wl
     dev = torch.device("cuda:0")
-    h_q, h_kv, d, B = 32, 4, 128, 4096
-    L = wl.VRSP_WINDOWS["256K"][0]
-    win = wl.vrsp_window("256K", gbs, seed)
+    h_q, h_kv, d = 32, 4, 128
+    L = wl.VRSP_WINDOWS[kind][0]
+    win = wl.vrsp_window(kind, gbs, seed)
     order, pool_load, _ = pl.libra_vrsp(win, pool_packs)
     k_top = int(np.argmax(pool_load))
     packs = [win[int(j)] for j in order[k_top * pool_packs:(k_top + 1) * pool_packs]]
@@ -293,8 +295,14 @@ def straggler_pool_bench(pool_packs: int = 8, cp: int = 8, seed: int = 1, gbs: i
     n_all = len(packs) * L
     g = torch.Generator(device=dev).manual_seed(12)
 
-    def rnd(shape):
-        return torch.randn(shape, device=dev, generator=g, dtype=torch.float32).to(torch.bfloat16)
+    def rnd(shape, chunk=1 << 20):
+        """bf16 N(0, 1), drawn in fp32 a million rows at a time (bounded temporaries)."""
+        out = torch.empty(shape, dtype=torch.bfloat16, device=dev)
+        for i in range(0, shape[0], chunk):
+            rows = min(chunk, shape[0] - i)
+            out[i:i + rows] = torch.randn((rows,) + tuple(shape[1:]), device=dev, generator=g,
+                                          dtype=torch.float32).to(torch.bfloat16)
+        return out
 
     q, k, v, do = rnd((n_all, h_q, d)), rnd((n_all, h_kv, d)), rnd((n_all, h_kv, d)), \
         rnd((n_all, h_q, d))
@@ -317,7 +325,7 @@ def straggler_pool_bench(pool_packs: int = 8, cp: int = 8, seed: int = 1, gbs: i
         t["q_row"] = t["q_begin"]
         return t
 
-    def run_set(tiles, reps=2):
+    def run_set(tiles):
         assert 0 < len(tiles) <= max_tiles
         td = pl.tiles_to_device(tiles, dev)
         best = None
@@ -360,16 +368,15 @@ def straggler_pool_bench(pool_packs: int = 8, cp: int = 8, seed: int = 1, gbs: i
     print(json.dumps({"libra_workers_done": len(lib)}), file=sys.stderr, flush=True)
     su, sz, sl = summary(uly), summary(zig), summary(lib)
     pack_work = [sum(x * x for x in pk) for pk in packs]
-    out = {"metric": "one-GPU straggler emulation, VRSP pool of 8 packs of 262,144 tokens, "
-                     "CP=8, 64 workers (fwd+bwd)",
+    out = {"metric": f"one-GPU straggler emulation, VRSP pool of {len(packs)} packs of {L:,} "
+                     f"tokens, CP={cp}, {len(packs) * cp} workers (fwd+bwd)",
            "value": round(su["max_ms"] / sl["max_ms"], 3),
            "unit": "x (head-parallel CP straggler / Libra straggler)",
            "higher_is_better": True, "data": "synthetic",
-           "config": {"window": f"{gbs} packs of {L} tokens, 0.95 lognormal(644, 1.5) + "
-                                f"0.05 Pareto(1.1, 8192), seed {seed}",
+           "config": {"window": f"{gbs} packs of {L} tokens ({kind} stand-in law), seed {seed}",
                       "pool": f"the heaviest of {len(pool_load)} Algorithm 1 pools of "
                               f"{pool_packs}", "h_q": h_q, "h_kv": h_kv, "head_dim": d,
-                      "cp": cp, "block_tokens": B, "head_shards": 2},
+                      "cp": cp, "block_tokens": B, "head_shards": 2, "best_of": reps},
            "pack_sum_l2_max_over_mean": round(max(pack_work) / float(np.mean(pack_work)), 4),
            "zigzag_straggler_over_libra": round(sz["max_ms"] / sl["max_ms"], 3),
            "ulysses": dict(su, ranks_timed=uly),
@@ -556,7 +563,10 @@ def main():
         straggler_bench()
         return
     if args.straggler_pool:
-        straggler_pool_bench()
+        if args.straggler_pool == "1M":
+            straggler_pool_bench("1M", pool_packs=4, cp=16, gbs=32, B=8192, reps=1)
+        else:
+            straggler_pool_bench()
         return
     if args.simulate:
         simulate()
