@@ -259,3 +259,49 @@ def test_out_of_range_tiles_are_skipped():
     assert skip1 == (3, 3), skip1
     for name, a, b in zip(("O", "LSE", "dQ", "dK", "dV"), ref, got):
         assert np.array_equal(a, b), f"{name} changed when out-of-range tiles were added"
+
+
+def _split_and_shuffle(tiles, seed):
+    """The same (row, head) pairs as `tiles`, cut into pieces of very different
+    lengths (single rows beside long remainders) and listed in shuffled order."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for t in tiles:
+        n = int(t["q_end"] - t["q_begin"])
+        cuts = sorted(set([0, n] + ([1, int(rng.integers(1, n))] if n > 2 else [])))
+        for a, b in zip(cuts[:-1], cuts[1:]):
+            p = t.copy()
+            p["q_begin"], p["q_end"], p["q_row"] = t["q_begin"] + a, t["q_begin"] + b, t["q_row"] + a
+            out.append(p)
+    out = np.array(out, dtype=pl.TILE_DTYPE)
+    return out[rng.permutation(len(out))]
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_fwd_bwd_ragged_shuffled_tiles(seed):
+    """Work items are built by 32-row windows of the longest tile: tiles of one
+    row next to long ones, in any list order, still cover every pair once."""
+    w = wl.small_random(100 + seed)
+    tiles = _split_and_shuffle(plan(w)[0], seed)
+    say(f"[ragged tiles {seed}] packs={w.pack_tokens} n={len(w.lengths)} "
+        f"heads=({w.h_q},{w.h_kv}) d={w.d} tiles={len(tiles)} "
+        f"lengths {int((tiles['q_end'] - tiles['q_begin']).min())}.."
+        f"{int((tiles['q_end'] - tiles['q_begin']).max())}")
+    q, k, v, do = _inputs(w)
+    qd, kd, vd, dod = _dev(q, k, v, do)
+    cu = cu_dev(w)
+    td = pl.tiles_to_device(tiles, DEV)
+    o, lse = pl.libra_attn_fwd(qd, kd, vd, cu, td)
+    dk32 = torch.zeros(kd.shape, dtype=torch.float32, device=DEV)
+    dv32 = torch.zeros_like(dk32)
+    dq, _, _ = pl.libra_attn_bwd(qd, kd, vd, o, lse, dod, cu, td, dk=dk32, dv=dv32,
+                                 accumulate=True)
+    torch.cuda.synchronize()
+    O, LSE = oa.attention_fwd(q, k, v, w.lengths, w.q_positions())
+    dQ, dK, dV = oa.attention_bwd(q, k, v, do, w.lengths, w.q_positions())
+    _, bq, bk, bv = attention_bf16(q, k, v, do, w.lengths)
+    check("O", to_np(o), O, bf16_out=True)
+    check("LSE", to_np(lse), LSE, (LSE_TOL, 1e-4))
+    check("dQ", to_np(dq), dQ, bf16_out=True, ref_bf16=bq)
+    check("dK fp32", to_np(dk32), dK, ref_bf16=bk)
+    check("dV fp32", to_np(dv32), dV, ref_bf16=bv)
