@@ -541,10 +541,14 @@ def cpu_baseline(w, q, k, v, do, seconds):
     dt = time.perf_counter() - t0
     pairs = oa.useful_pairs(w.lengths, pos[np.asarray(done_rows, dtype=np.int64)])
     flops = 14.0 * w.d * w.h_q * pairs
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": torch.get_num_threads(),
+    rate = flops / dt / 1e12
+    full_pairs = oa.useful_pairs(w.lengths, pos)
+    return {"value": rate, "unit": "TFLOP/s", "cores": torch.get_num_threads(),
             "kind": "oracle",
             "sample": (f"{len(done_rows)} random query rows of {len(pos)} x {w.h_q} heads, "
-                       f"fwd+bwd in float64 ({pairs} causal pairs per head, {dt:.1f} s)")}
+                       f"fwd+bwd in float64 ({pairs} causal pairs per head, {dt:.1f} s)"),
+            # the whole step's useful work at the sampled rate (extrapolated, not timed)
+            "extrapolated_step_s": round(14.0 * w.d * w.h_q * full_pairs / 1e12 / rate, 1)}
 
 
 def main():
