@@ -49,8 +49,11 @@ def parse():
                     help="one of the seeded workloads: 4K-h2-kv1-d64, 32K-qwen3-8b, "
                          "pool8x64K-qwen3-30b-a3b, 256K-cp16-share-qwen3-235b-a22b, "
                          "1M-cp16-share-qwen3-30b-a3b")
+    ap.add_argument("--cpu-rows", type=int, default=64,
+                    help="query rows of the fixed subset the CPU oracle baseline runs on "
+                         "(0 disables it)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
-                    help="time budget of the CPU oracle baseline (0 disables it)")
+                    help="time budget of the oracle baseline of --vrsp")
     ap.add_argument("--vrsp", action="store_true",
                     help="only measure Variance-Reduced Sequence Placement (Algorithm 1) on the "
                          "host: time per GBS window and the inter-pool imbalance R - 1 against "
@@ -515,38 +518,62 @@ def mfma_loop_peak(pl, torch, dev):
             "kind": "independent v_mfma_f32_32x32x16_bf16 products, no other work"}
 
 
-def cpu_baseline(w, q, k, v, do, seconds):
-    """The oracle, as it stands, on a bounded random sample of query rows of the
-    same workload (all heads, forward + backward)."""
+def _cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_rows(w, n_rows: int) -> np.ndarray:
+    """The fixed CPU-baseline row subset: 1/8 of the rows evenly spaced over
+    the present rows of the longest sample (the straggler rows, each attending
+    up to the whole sample), the rest evenly spaced over all other rows."""
+    pos = w.q_positions()
+    cu = np.concatenate([[0], np.cumsum(w.lengths)])
+    j_long = int(np.argmax(w.lengths))
+    in_long = (pos >= cu[j_long]) & (pos < cu[j_long + 1])
+    longs, others = np.nonzero(in_long)[0], np.nonzero(~in_long)[0]
+    n_long = min(len(longs), max(1, n_rows // 8))
+    n_other = min(len(others), n_rows - n_long)
+    pick = [longs[np.linspace(0, len(longs) - 1, n_long).round().astype(np.int64)]] if n_long else []
+    if n_other:
+        pick.append(others[np.linspace(0, len(others) - 1, n_other).round().astype(np.int64)])
+    return np.unique(np.concatenate(pick))
+
+
+def cpu_baseline(w, q, k, v, do, n_rows):
+    """The oracle, as it stands, on a fixed subset of query rows of the same
+    workload (all heads, forward + backward, one call each: the oracle groups
+    the rows by sample itself)."""
     import torch
     from oracle import attention as oa
     pos = w.q_positions()
-    rng = np.random.default_rng(12345)
-    order = rng.permutation(len(pos))
-    done_rows = []
+    rows = cpu_rows(w, n_rows)
     t0 = time.perf_counter()
-    i = 0
-    # one row at a time; stop before a row that, at the mean time per row so
-    # far, would end past the budget (rows differ a lot: a row attends its
-    # sample's preceding keys, up to the whole 900K-token sample)
-    while i < len(order):
-        el = time.perf_counter() - t0
-        if done_rows and el + el / len(done_rows) > seconds:
-            break
-        rows = order[i:i + 1]
-        i += 1
-        oa.attention_fwd(q, k, v, w.lengths, pos, rows=rows)
-        oa.attention_bwd(q, k, v, do, w.lengths, pos, rows=rows)
-        done_rows.extend(rows.tolist())
+    oa.attention_fwd(q, k, v, w.lengths, pos, rows=rows)
+    oa.attention_bwd(q, k, v, do, w.lengths, pos, rows=rows)
     dt = time.perf_counter() - t0
-    pairs = oa.useful_pairs(w.lengths, pos[np.asarray(done_rows, dtype=np.int64)])
+    pairs = oa.useful_pairs(w.lengths, pos[rows])
     flops = 14.0 * w.d * w.h_q * pairs
     rate = flops / dt / 1e12
     full_pairs = oa.useful_pairs(w.lengths, pos)
-    return {"value": rate, "unit": "TFLOP/s", "cores": torch.get_num_threads(),
+    cu = np.concatenate([[0], np.cumsum(w.lengths)])
+    j_long = int(np.argmax(w.lengths))
+    n_long = int(((pos[rows] >= cu[j_long]) & (pos[rows] < cu[j_long + 1])).sum())
+    return {"value": rate, "unit": "TFLOP/s",
+            "cores": len(os.sched_getaffinity(0)),
+            "blas_threads": torch.get_num_threads(),
+            "cpu_model": _cpu_model(),
             "kind": "oracle",
-            "sample": (f"{len(done_rows)} random query rows of {len(pos)} x {w.h_q} heads, "
-                       f"fwd+bwd in float64 ({pairs} causal pairs per head, {dt:.1f} s)"),
+            "sample": (f"fixed subset of {len(rows)} of {len(pos)} query rows x {w.h_q} heads "
+                       f"({n_long} rows of the longest sample, {len(rows) - n_long} spread over "
+                       f"the others), fwd+bwd in float64: {pairs} causal pairs per head in "
+                       f"{dt:.1f} s"),
+            "seconds": round(dt, 2),
             # the whole step's useful work at the sampled rate (extrapolated, not timed)
             "extrapolated_step_s": round(14.0 * w.d * w.h_q * full_pairs / 1e12 / rate, 1)}
 
@@ -750,8 +777,8 @@ def main():
     loop = mfma_loop_peak(pl, torch, dev)
     out["mfma_loop_peak"] = loop
     out["roofline"]["frac_of_mfma_loop_peak"] = round(achieved / loop["value"], 4)
-    if args.cpu_seconds > 0:
-        out["cpu_baseline"] = cpu_baseline(w, q, k, v, do, args.cpu_seconds)
+    if args.cpu_rows > 0:
+        out["cpu_baseline"] = cpu_baseline(w, q, k, v, do, args.cpu_rows)
     print(json.dumps(out), flush=True)
 
 

@@ -180,6 +180,29 @@ int libra_attn_fwd(const void *q, const void *k, const void *v, const int64_t *c
                    int32_t head_dim, float softmax_scale, void *o, float *lse, void *workspace,
                    size_t workspace_bytes, void *stream);
 
+/*
+ * Tiles that do not lie inside the buffers a call describes (q_begin < 0,
+ * q_end > n_kv_rows, empty ranges, rows past n_q_rows, heads outside
+ * [0, h_q)) are skipped on the device: the call still returns LIBRA_OK and
+ * computes every other tile exactly as without them.  The number skipped by
+ * the last libra_attn_fwd or libra_attn_bwd call that used a workspace is an
+ * int32 at byte offset LIBRA_WS_SKIPPED_OFFSET of that workspace (plus 1 if
+ * the workspace's work-item list overflowed, which a workspace of
+ * libra_attn_workspace_size bytes rules out).
+ *
+ * libra_attn_skipped_tiles -- copies that count to *count after the work
+ * already enqueued on `stream` has finished (it synchronizes `stream`).
+ *   workspace: the device workspace of that call (256-byte aligned).
+ * Errors: EINVAL (NULL arguments), EHIP.
+ *
+ * Tiles that overlap in (row, head) are not detected.  Each copy is computed
+ * in full: O, LSE and dQ of the shared pairs are written twice with the same
+ * values, and dK / dV receive their contribution twice.  libra_plan never
+ * produces overlapping tiles.
+ */
+#define LIBRA_WS_SKIPPED_OFFSET 16
+int libra_attn_skipped_tiles(const void *workspace, int32_t *count, void *stream);
+
 /* libra_attn_bwd flags */
 #define LIBRA_BWD_ACCUMULATE_DKV 1u /* dk, dv are fp32 and are added to (not overwritten) */
 
@@ -198,6 +221,14 @@ int libra_attn_fwd(const void *q, const void *k, const void *v, const int64_t *c
  *       this call's contribution is added, so several disjoint tile sets
  *       (virtual workers) can be summed into one caller-zeroed buffer.
  *   workspace: >= libra_attn_workspace_size(..., 1) bytes, 256-byte aligned.
+ * Precision: the dK / dV products take fp16 copies of q, dout, k and v, each
+ * scaled by a power of two from its max |x| over what the products read, so
+ * that P and dS round to 11 significant bits instead of bf16's 8; the scales
+ * are undone exactly on output.  dQ's products take the bf16 inputs.
+ * Inputs: every element of k and v in the samples the tiles touch, and of
+ * q, dout, o and lse in the covered (row, head) pairs, must be finite.
+ * Other rows of q, dout, o and lse are not read by the dK / dV products
+ * (their fp16 copies hold zeros there).
  */
 int libra_attn_bwd(const void *q, const void *k, const void *v, const void *o, const float *lse,
                    const void *dout, const int64_t *cu_seqlens, int64_t num_samples,

@@ -9,8 +9,6 @@ library computes, written from the paper (Libra, arXiv 2607.23250):
 * ``oracle.attention`` -- document-masked causal attention (Eq. 1 under the
   block-diagonal causal mask of Sec. 2.3), forward and backward, in float64
   (torch CPU), one sample and one head at a time.
-* ``oracle.bf16_reference`` -- the same attention in plain bf16 PyTorch, used
-  only for the error allowance of the paper's fidelity criterion (Sec. 6.7).
 * ``oracle.vrsp``      -- Variance-Reduced Sequence Placement (Algorithm 1,
   Eq. 4) and the inter-pool imbalance R - 1 of Sec. 3.2, in Python integers.
 

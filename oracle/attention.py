@@ -113,7 +113,7 @@ def attention_fwd(q, k, v, lengths: Sequence[int], q_pos, scale: Optional[float]
 
 
 def attention_bwd(q, k, v, dout, lengths: Sequence[int], q_pos,
-                  scale: Optional[float] = None, rows=None, kv_heads=None):
+                  scale: Optional[float] = None, rows=None, kv_heads=None, dkdv: bool = True):
     """Backward oracle: gradients of sum(dO * O) with respect to Q, K, V.
 
     Only the requested ``rows`` contribute (for a ``dout`` that is zero on
@@ -121,7 +121,9 @@ def attention_bwd(q, k, v, dout, lengths: Sequence[int], q_pos,
     computation to the query heads of those KV heads.  Returns
     ``(dQ, dK, dV)`` in float64: dQ [R, h_q, d] for the R requested rows in
     the order given (every row when ``rows`` is None; NaN for heads not
-    computed), dK / dV [N_k, h_kv, d] (views of per-KV-head arrays).
+    computed), dK / dV [N_k, h_kv, d] (views of per-KV-head arrays).  With
+    ``dkdv=False`` the dK / dV sums are skipped (they stay zero); dQ is the
+    same.
     """
     n_q, h_q, d = q.shape
     n_k, h_kv, _ = k.shape
@@ -154,11 +156,13 @@ def attention_bwd(q, k, v, dout, lengths: Sequence[int], q_pos,
                     Pm = torch.exp(S - lse[:, None])            # softmax rows
                     Oc = Pm @ Vj
                     D = (dOc * Oc).sum(dim=1)
-                    dV[g, s:s + n_keys, :] += (Pm.T @ dOc).numpy()
+                    if dkdv:
+                        dV[g, s:s + n_keys, :] += (Pm.T @ dOc).numpy()
                     dP = dOc @ Vj.T
                     dS = Pm * (dP - D[:, None])
                     dQ[pl.out[rc], hq, :] = ((dS @ Kj) * scale).numpy()
-                    dK[g, s:s + n_keys, :] += ((dS.T @ Qc) * scale).numpy()
+                    if dkdv:
+                        dK[g, s:s + n_keys, :] += ((dS.T @ Qc) * scale).numpy()
     return dQ, np.moveaxis(dK, 0, 1), np.moveaxis(dV, 0, 1)
 
 

@@ -34,7 +34,8 @@ assert TILE_DTYPE.itemsize == 56
 EXPORTED = ("libra_strerror", "libra_last_error", "libra_plan", "libra_vrsp",
             "libra_attn_workspace_size", "libra_attn_fwd", "libra_attn_bwd",
             "libra_timing_enable", "libra_timing_read", "libra_mfma_loop_size",
-            "libra_mfma_loop")
+            "libra_mfma_loop", "libra_attn_skipped_tiles")
+LIBRA_WS_SKIPPED_OFFSET = 16
 
 
 class LibraError(RuntimeError):
@@ -88,6 +89,8 @@ def lib() -> ctypes.CDLL:
                                        ctypes.POINTER(ctypes.c_int64)]
     L.libra_mfma_loop.restype = ctypes.c_int
     L.libra_mfma_loop.argtypes = [I32, I32, P, I64, P]
+    L.libra_attn_skipped_tiles.restype = ctypes.c_int
+    L.libra_attn_skipped_tiles.argtypes = [P, ctypes.POINTER(ctypes.c_int32), P]
     _lib = L
     return L
 
@@ -256,6 +259,15 @@ def libra_attn_fwd(q, k, v, cu_seqlens, tiles, *, softmax_scale: float = 0.0, o=
                                 o.data_ptr(), lse.data_ptr(), workspace.data_ptr(),
                                 workspace.numel(), _stream(q.device)), "libra_attn_fwd")
     return o, lse
+
+
+def libra_attn_skipped_tiles(workspace) -> int:
+    """Tiles skipped as out of range by the last fwd / bwd call that used
+    ``workspace`` (synchronizes the current stream)."""
+    n = ctypes.c_int32(0)
+    _check(lib().libra_attn_skipped_tiles(workspace.data_ptr(), ctypes.byref(n),
+                                          _stream(workspace.device)), "libra_attn_skipped_tiles")
+    return int(n.value)
 
 
 def libra_mfma_loop(waves_per_simd: int, iters: int, record) -> None:

@@ -127,6 +127,19 @@ extern "C" int libra_attn_fwd(const void *q, const void *k, const void *v,
                     static_cast<hipStream_t>(stream), tm);
 }
 
+extern "C" int libra_attn_skipped_tiles(const void *workspace, int32_t *count, void *stream) {
+  last_error_text().clear();
+  if (!workspace || !count) return fail(LIBRA_EINVAL, "NULL workspace or count");
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  int32_t v = 0;
+  if (hipMemcpyAsync(&v, static_cast<const char *>(workspace) + LIBRA_WS_SKIPPED_OFFSET,
+                     sizeof(v), hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return fail(LIBRA_EHIP, "reading the skipped-tile count failed");
+  *count = v;
+  return LIBRA_OK;
+}
+
 extern "C" int libra_attn_bwd(const void *q, const void *k, const void *v, const void *o,
                               const float *lse, const void *dout, const int64_t *cu_seqlens,
                               int64_t num_samples, const libra_tile_t *tiles, int64_t num_tiles,

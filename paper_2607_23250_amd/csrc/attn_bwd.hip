@@ -67,11 +67,20 @@ __global__ __launch_bounds__(kPrepThreads) void prep_bwd_kernel(
     __hip_atomic_store(&ext[j], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&gmask[j], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
+  if (tid < 5) {
+    // the skipped-tile count (counted here for the backward) and the max |x| slots
+    __hip_atomic_store(&hdr[tid == 0 ? (int)kBadTiles : kMaxAbs + tid - 1], 0, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  }
   __threadfence();
   __syncthreads();
+  int bad = 0;
   for (int64_t t = tid; t < T; t += kPrepThreads) {
     const libra_tile_t tl = tiles[t];
-    if (!tile_ok(tl, n_q, n_kv, h_q)) continue;
+    if (!tile_ok(tl, n_q, n_kv, h_q)) {
+      ++bad;
+      continue;
+    }
     const unsigned long long bits = group_bits(tl.head_begin, tl.head_end, G);
     for (int64_t j = upper_bound64(cu, n, tl.q_begin) - 1; j < n && cu[j] < tl.q_end; ++j) {
       const int64_t pe = tl.q_end < cu[j + 1] ? tl.q_end : cu[j + 1];
@@ -79,6 +88,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_bwd_kernel(
       atomicOr(&gmask[j], bits);
     }
   }
+  if (bad) atomicAdd(&hdr[kBadTiles], bad);
   __threadfence();
   __syncthreads();
   // Samples with more than kCoopBlocks key blocks are enumerated by the
@@ -129,28 +139,148 @@ __global__ __launch_bounds__(kPrepThreads) void prep_bwd_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Pre-pass over the covered (row, head) pairs, 32 rows at a time: per 32-row
-// block of each head the 32 values LSE * log2(e) followed by the 32 values
-// D = rowsum(dO * O) ("stats", [h_q][nq_pad / 32][64] floats, so one
-// 256-byte load fetches both), and for the dK / dV kernel the same two
-// quantities as one extra 16-deep k-block of the S and dP products ("aug",
-// [h_q][nq_pad / 32][2][64 lanes][8] bf16): MFMA A-operand lane l < 32 holds
-// three bf16 terms summing to -LSE / scale (first record) or -D (second) of
-// the block's row perm32(l), then zeros; lanes 32..63 hold zeros.  Against a
-// B operand of ones in k = 0, 1, 2 the products then come out as S - LSE / scale
-// and dP - D directly.
+// fp16 operands of the dK / dV kernel.  Its products run on fp16 copies of
+// Q, dO, K and V (same matrix-core rate as bf16, three more significant bits
+// for the rounded P and dS operands), each scaled by a power of two chosen
+// from the tensor's max |x| over what the kernel reads (fp16_scale), so that
+// the copies stay inside the fp16 range whatever the inputs' magnitude.
+// Two passes find the maxima (fp32 bits, atomicMax on the header slots
+// kMaxAbs + 0..3): Q and dO over the covered (row, head) pairs, K and V over
+// the keys of the dK / dV work items.
+
+// Wave-wide max of non-negative floats, then one atomic per wave.
+__device__ __forceinline__ void wave_max_to(float m, int32_t *slot) {
+  for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+  if ((threadIdx.x & 63) == 0 && m > 0.f)
+    atomicMax(reinterpret_cast<unsigned int *>(slot), __float_as_uint(m));
+}
+
+__device__ __forceinline__ float absmax8(const bf16x8 &x) {
+  float m = 0.f;
+  static_for<8>([&](auto i) { m = fmaxf(m, fabsf(static_cast<float>(x[int(i)]))); });
+  return m;
+}
+
 constexpr int kTileSplit = 64;
-constexpr int kAugEl = 2 * 64 * 8;   // bf16 elements of one block's two records
 
-
+// Per tile (kTileSplit workgroups each): max |Q| and max |dO| over the
+// covered (row, head) pairs; and, in the fp16 copies, zeros for the rows of
+// the tile's first and last 32-row blocks that lie outside the tile (the
+// dK / dV kernel stages whole blocks; rows no tile covers must hold finite
+// values, since they meet P = dS = 0 in its products).
 template <int D>
-__global__ __launch_bounds__(256) void bwd_pre_kernel(
-    const bf16 *__restrict__ o, const bf16 *__restrict__ dout, const float *__restrict__ lse,
+__global__ __launch_bounds__(256) void bwd_absmax_q_kernel(
+    const bf16 *__restrict__ q, const bf16 *__restrict__ dout,
     const libra_tile_t *__restrict__ tiles, int h_q, int64_t n_q, int64_t n_kv,
-    int64_t nq_pad, float scale, float *__restrict__ stats, bf16 *__restrict__ aug) {
+    int32_t *__restrict__ hdr, f16 *__restrict__ q16, f16 *__restrict__ do16) {
   const int tid = threadIdx.x;
   const libra_tile_t tl = tiles[blockIdx.x / kTileSplit];
   if (!tile_ok(tl, n_q, n_kv, h_q)) return;
+  const int64_t ra = tl.q_row, rb = tl.q_row + (tl.q_end - tl.q_begin);
+  const int r = tid >> 3, part = tid & 7;   // 8 threads per row, 32 rows per pass
+  float mq = 0.f, mo = 0.f;
+  for (int64_t m = ra / kRows + blockIdx.x % kTileSplit; m * kRows < rb; m += kTileSplit) {
+    const int64_t row = m * kRows + r;
+    const bool ok = row >= ra && row < rb;
+    if (!ok && row >= n_q) continue;
+    for (int h = tl.head_begin; h < tl.head_end; ++h) {
+      const size_t off = ((size_t)row * h_q + h) * D + part * (D / 8);
+      static_for<D / 64>([&](auto c) {
+        if (ok) {
+          mq = fmaxf(mq, absmax8(*reinterpret_cast<const bf16x8 *>(q + off + 8 * c)));
+          mo = fmaxf(mo, absmax8(*reinterpret_cast<const bf16x8 *>(dout + off + 8 * c)));
+        } else {
+          f16x8 z;
+          static_for<8>([&](auto i) { z[int(i)] = f16(0.f); });
+          *reinterpret_cast<f16x8 *>(q16 + off + 8 * c) = z;
+          *reinterpret_cast<f16x8 *>(do16 + off + 8 * c) = z;
+        }
+      });
+    }
+  }
+  wave_max_to(mq, &hdr[kMaxAbs + 0]);
+  wave_max_to(mo, &hdr[kMaxAbs + 1]);
+}
+
+// The keys the dK / dV kernel loads: for every sample with covered rows,
+// its keys up to the end of the last 128-key block that those rows attend
+// (all KV heads).  One wave per key row.  CONVERT = false: max |K| and
+// max |V| over them; CONVERT = true: their scaled fp16 copies.
+template <int D, bool CONVERT>
+__global__ __launch_bounds__(256) void bwd_kv_pass_kernel(
+    const bf16 *__restrict__ k, const bf16 *__restrict__ v, const int64_t *__restrict__ cu,
+    int64_t n, const int32_t *__restrict__ ext, int h_kv, int64_t n_kv,
+    int32_t *__restrict__ hdr, f16 *__restrict__ k16, f16 *__restrict__ v16) {
+  const int l = threadIdx.x & 63;
+  const int64_t wave = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 6;
+  const int64_t waves = (int64_t)gridDim.x * 4;
+  const int chunks = h_kv * D / 8;   // 16-byte chunks of a row
+  float mk = 0.f, mv = 0.f, s_k = 1.f, s_v = 1.f;
+  if constexpr (CONVERT) {
+    s_k = fp16_scale((uint32_t)hdr[kMaxAbs + 2], false);
+    s_v = fp16_scale((uint32_t)hdr[kMaxAbs + 3], true);
+  }
+  int64_t lo = 0, hi = 0, end = 0;   // rows [lo, hi) of the current sample; loaded keys end at `end`
+  for (int64_t row = wave; row < n_kv; row += waves) {
+    if (row < lo || row >= hi) {
+      const int64_t j = upper_bound64(cu, n, row) - 1;
+      lo = cu[j];
+      hi = cu[j + 1];
+      const int64_t e = (int64_t)ext[j];
+      const int64_t lim = (e + kBwdBK - 1) / kBwdBK * kBwdBK;
+      end = lo + (e > 0 ? (lim < hi - lo ? lim : hi - lo) : 0);
+    }
+    if (row >= end) continue;
+    for (int c = l; c < chunks; c += 64) {
+      const size_t off = (size_t)row * h_kv * D + 8 * (size_t)c;
+      const bf16x8 kx = *reinterpret_cast<const bf16x8 *>(k + off);
+      const bf16x8 vx = *reinterpret_cast<const bf16x8 *>(v + off);
+      if constexpr (CONVERT) {
+        f16x8 kh, vh;
+        static_for<8>([&](auto i) {
+          kh[int(i)] = static_cast<f16>(static_cast<float>(kx[int(i)]) * s_k);
+          vh[int(i)] = static_cast<f16>(static_cast<float>(vx[int(i)]) * s_v);
+        });
+        *reinterpret_cast<f16x8 *>(k16 + off) = kh;
+        *reinterpret_cast<f16x8 *>(v16 + off) = vh;
+      } else {
+        mk = fmaxf(mk, absmax8(kx));
+        mv = fmaxf(mv, absmax8(vx));
+      }
+    }
+  }
+  if constexpr (!CONVERT) {
+    wave_max_to(mk, &hdr[kMaxAbs + 2]);
+    wave_max_to(mv, &hdr[kMaxAbs + 3]);
+  }
+}
+
+// Pre-pass over the covered (row, head) pairs, 32 rows at a time:
+//   * the fp16 copies of Q and dO (scaled, see above);
+//   * per 32-row block of each head, the 32 values LSE * log2(e) followed by
+//     the 32 values D = rowsum(dO * O) for the dQ kernel ("stats",
+//     [h_q][nq_pad / 32][64] floats, so one 256-byte load fetches both);
+//   * for the dK / dV kernel the first of the two records of its extra
+//     16-deep k-block ("aug", [h_q][nq_pad / 32][2][64 lanes][8] fp16): MFMA
+//     A-operand lane l < 32 holds three fp16 terms summing to -LSE / scale
+//     (first record) or -D (second, written by the dQ kernel from the exact
+//     row sums) of the block's row perm32(l), in the scaled units of the
+//     copies, then zeros; lanes 32..63 hold zeros.  Against a B operand of
+//     ones in k = 0, 1, 2 the products then come out as S - LSE / scale and
+//     dP - D directly.
+template <int D>
+__global__ __launch_bounds__(256) void bwd_pre_kernel(
+    const bf16 *__restrict__ q, const bf16 *__restrict__ o, const bf16 *__restrict__ dout,
+    const float *__restrict__ lse, const libra_tile_t *__restrict__ tiles, int h_q,
+    int64_t n_q, int64_t n_kv, int64_t nq_pad, float scale, const int32_t *__restrict__ hdr,
+    f16 *__restrict__ q16, f16 *__restrict__ do16, float *__restrict__ stats,
+    f16 *__restrict__ aug) {
+  const int tid = threadIdx.x;
+  const libra_tile_t tl = tiles[blockIdx.x / kTileSplit];
+  if (!tile_ok(tl, n_q, n_kv, h_q)) return;
+  const float s_q = fp16_scale((uint32_t)hdr[kMaxAbs + 0], false);
+  const float s_o = fp16_scale((uint32_t)hdr[kMaxAbs + 1], true);
+  const float s_k = fp16_scale((uint32_t)hdr[kMaxAbs + 2], false);
   const int64_t ra = tl.q_row, rb = tl.q_row + (tl.q_end - tl.q_begin);
   // 8 threads per row, 32 rows per pass
   const int r = tid >> 3, part = tid & 7;
@@ -162,11 +292,18 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(
       if (ok) {
         const size_t off = ((size_t)row * h_q + h) * D + part * (D / 8);
         static_for<D / 64>([&](auto c) {
+          const bf16x8 qv = *reinterpret_cast<const bf16x8 *>(q + off + 8 * c);
           const bf16x8 ov = *reinterpret_cast<const bf16x8 *>(o + off + 8 * c);
           const bf16x8 dv = *reinterpret_cast<const bf16x8 *>(dout + off + 8 * c);
+          f16x8 qh, dh;
           static_for<8>([&](auto i) {
-            acc += static_cast<float>(ov[int(i)]) * static_cast<float>(dv[int(i)]);
+            const float dx = static_cast<float>(dv[int(i)]);
+            acc += static_cast<float>(ov[int(i)]) * dx;
+            qh[int(i)] = static_cast<f16>(static_cast<float>(qv[int(i)]) * s_q);
+            dh[int(i)] = static_cast<f16>(dx * s_o);
           });
+          *reinterpret_cast<f16x8 *>(q16 + off + 8 * c) = qh;
+          *reinterpret_cast<f16x8 *>(do16 + off + 8 * c) = dh;
         });
       }
       acc += __shfl_xor(acc, 1);
@@ -177,12 +314,10 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(
         const float lv = lse[(size_t)h * n_q + row];
         st[r] = lv * kLog2e;
         st[kRows + r] = acc;
-        bf16 *ag = aug + ((size_t)h * (nq_pad / kRows) + m) * kAugEl + 8 * perm32(r);
-        bf16x8 sv, dv;
-        split3(-lv / scale, sv);
-        split3(-acc, dv);
-        *reinterpret_cast<bf16x8 *>(ag) = sv;
-        *reinterpret_cast<bf16x8 *>(ag + kAugEl / 2) = dv;
+        f16 *ag = aug + ((size_t)h * (nq_pad / kRows) + m) * kAugEl + 8 * perm32(r);
+        f16x8 sv;
+        split3h(-lv / scale * (s_q * s_k), sv);
+        *reinterpret_cast<f16x8 *>(ag) = sv;
       }
     }
   }
@@ -290,8 +425,8 @@ struct StepIter {
 
 template <int D>
 __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) void attn_bwd_dkdv_kernel(
-    const bf16 *__restrict__ k, const bf16 *__restrict__ v, const bf16 *__restrict__ q,
-    const bf16 *__restrict__ dout, const bf16 *__restrict__ aug,
+    const f16 *__restrict__ k, const f16 *__restrict__ v, const f16 *__restrict__ q,
+    const f16 *__restrict__ dout, const f16 *__restrict__ aug,
     const int64_t *__restrict__ cu, const libra_tile_t *__restrict__ tiles, int64_t T,
     const BwdItem *__restrict__ items, int32_t *__restrict__ hdr, int h_q, int h_kv,
     int64_t n_q, int64_t n_kv, int64_t nq_pad, float scale, float c2,
@@ -331,8 +466,18 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
     q_lane[u] = 2u * (uint32_t)(r * h_q * D + 8 * swt<S::QC>(r, l % S::QC));
   });
   // B operand of the augmented k-block: ones in k = 0, 1, 2 (lanes of kg 0)
-  bf16x8 ones3;
-  static_for<8>([&](auto i) { ones3[int(i)] = bf16(kg == 0 && i < 3 ? 1.f : 0.f); });
+  f16x8 ones3;
+  static_for<8>([&](auto i) { ones3[int(i)] = f16(kg == 0 && i < 3 ? 1.f : 0.f); });
+  // Every operand is an fp16 copy scaled by a power of two (fp16_scale): the
+  // scores come out multiplied by s_q s_k, dP and D by s_o s_v, so the
+  // exponent takes c2 / (s_q s_k) and the outputs are scaled back at the end
+  // (exactly: all factors are powers of two).
+  const float s_q = fp16_scale((uint32_t)hdr[kMaxAbs + 0], false);
+  const float s_o = fp16_scale((uint32_t)hdr[kMaxAbs + 1], true);
+  const float s_k = fp16_scale((uint32_t)hdr[kMaxAbs + 2], false);
+  const float s_v = fp16_scale((uint32_t)hdr[kMaxAbs + 3], true);
+  const float c2s = c2 / (s_q * s_k);
+  const float dk_mul = scale / (s_q * s_o * s_v), dv_mul = 1.f / s_o;
 
   for (;;) {
     if (tid == 0) s_item = take_item(hdr, kBwdQ, q_serve, q_left);
@@ -350,14 +495,14 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
     const bool wave_keys_ok = kw0 + 31 < len;
     const int64_t krow = key0 + kl;
 
-    bf16x8 kf[D / 16], vf[D / 16];
+    f16x8 kf[D / 16], vf[D / 16];
     static_for<D / 16>([&](auto c) {
       if (key_ok) {
         const size_t off = ((size_t)krow * h_kv + g) * D + 16 * c + 8 * kg;
-        kf[c] = *reinterpret_cast<const bf16x8 *>(k + off);
-        vf[c] = *reinterpret_cast<const bf16x8 *>(v + off);
+        kf[c] = *reinterpret_cast<const f16x8 *>(k + off);
+        vf[c] = *reinterpret_cast<const f16x8 *>(v + off);
       } else {
-        static_for<8>([&](auto i) { kf[c][int(i)] = bf16(0.f); vf[c][int(i)] = bf16(0.f); });
+        static_for<8>([&](auto i) { kf[c][int(i)] = f16(0.f); vf[c][int(i)] = f16(0.f); });
       }
     });
     wait_vm_known();
@@ -416,16 +561,16 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
       const bf16 *dOs = Qs + S::Q_EL;
       const bf16 *Ag = dOs + S::Q_EL;     // -LSE / scale record, then the -D record
       // (1) Q rows and this lane's part of the -LSE / scale operand
-      bf16x8 qa[NC], oa[NC], sag, dag;
-      sag = *reinterpret_cast<const bf16x8 *>(Ag + 8 * l);
-      static_for<NC>([&](auto c) { qa[c] = *reinterpret_cast<const bf16x8 *>(Qs + qoff[c]); });
+      f16x8 qa[NC], oa[NC], sag, dag;
+      sag = *reinterpret_cast<const f16x8 *>(Ag + 8 * l);
+      static_for<NC>([&](auto c) { qa[c] = *reinterpret_cast<const f16x8 *>(Qs + qoff[c]); });
       __builtin_amdgcn_sched_barrier(0);
       // (2) S - LSE / scale = [Q | aug] [K | ones]^T (queries on M, this
       // lane's key on N) while the dO rows and the -D operand load
-      f32x16 sa = mfma32(sag, ones3, mfma_zero_c()), pa;
-      static_for<NC>([&](auto c) { sa = mfma32(qa[c], kf[c], sa); });
-      dag = *reinterpret_cast<const bf16x8 *>(Ag + kAugEl / 2 + 8 * l);
-      static_for<NC>([&](auto c) { oa[c] = *reinterpret_cast<const bf16x8 *>(dOs + qoff[c]); });
+      f32x16 sa = mfma32h(sag, ones3, mfma_zero_c()), pa;
+      static_for<NC>([&](auto c) { sa = mfma32h(qa[c], kf[c], sa); });
+      dag = *reinterpret_cast<const f16x8 *>(Ag + kAugEl / 2 + 8 * l);
+      static_for<NC>([&](auto c) { oa[c] = *reinterpret_cast<const f16x8 *>(dOs + qoff[c]); });
       static_for<NC + 1>([&](auto i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, i < NC / 2 + 1 ? 2 : 0, 0);
@@ -434,29 +579,29 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
       // (3) dP - D = [dO | aug] [V | ones]^T with P = exp2((S - LSE / scale) c2)
       // on the VALU and the transpose reads of dO^T; register 8 hh + i of S
       // holds row 16 hh + 8 kg + i
-      bf16x8 ta[NT][2];
+      f16x8 ta[NT][2];
       float pf[16];
-      bf16x8 pb16[2], db16[2];
+      f16x8 pb16[2], db16[2];
       auto phase3 = [&](auto mask_t) {
       constexpr bool MASK = decltype(mask_t)::value;
-      pa = mfma32(dag, ones3, mfma_zero_c());
-      static_for<NC>([&](auto c) { pa = mfma32(oa[c], vf[c], pa); });
+      pa = mfma32h(dag, ones3, mfma_zero_c());
+      static_for<NC>([&](auto c) { pa = mfma32h(oa[c], vf[c], pa); });
       static_for<2>([&](auto hh) {
         static_for<8>([&](auto i) {
           constexpr int r = 8 * hh + i;
-          float p = fast_exp2(sa[r] * c2);
+          float p = fast_exp2(sa[r] * c2s);
           if constexpr (MASK) {
             const int iq = 16 * hh + 8 * kg + i;
             p = (iq >= lower && iq < upper) ? p : 0.f;
           }
           pf[r] = p;
-          pb16[hh][int(i)] = static_cast<bf16>(p);
+          pb16[hh][int(i)] = static_cast<f16>(p);
         });
       });
       static_for<NT>([&](auto dt) {
         static_for<2>([&](auto c) {
-          const bf16 *base = dOs + 16 * c * D;
-          ta[dt][c] = lds_tr16x2(base + troff[dt][0], base + troff[dt][1]);
+          const f16 *base = reinterpret_cast<const f16 *>(dOs) + 16 * c * D;
+          ta[dt][c] = lds_tr16x2h(base + troff[dt][0], base + troff[dt][1]);
         });
       });
       static_for<NC + 1>([&](auto i) {
@@ -470,20 +615,20 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
       __builtin_amdgcn_sched_barrier(0);
       // (4) dV^T += dO^T P with dS = P (dP - D) on the VALU and the transpose
       // reads of Q^T
-      bf16x8 tq[NT][2];
+      f16x8 tq[NT][2];
       static_for<NT>([&](auto dt) {
-        static_for<2>([&](auto c) { dva[dt] = mfma32(ta[dt][c], pb16[c], dva[dt]); });
+        static_for<2>([&](auto c) { dva[dt] = mfma32h(ta[dt][c], pb16[c], dva[dt]); });
       });
       static_for<2>([&](auto hh) {
         static_for<8>([&](auto i) {
           constexpr int r = 8 * hh + i;
-          db16[hh][int(i)] = static_cast<bf16>(pf[r] * pa[r]);
+          db16[hh][int(i)] = static_cast<f16>(pf[r] * pa[r]);
         });
       });
       static_for<NT>([&](auto dt) {
         static_for<2>([&](auto c) {
-          const bf16 *base = Qs + 16 * c * D;
-          tq[dt][c] = lds_tr16x2(base + troff[dt][0], base + troff[dt][1]);
+          const f16 *base = reinterpret_cast<const f16 *>(Qs) + 16 * c * D;
+          tq[dt][c] = lds_tr16x2h(base + troff[dt][0], base + troff[dt][1]);
         });
       });
       static_for<2 * NT>([&](auto i) {
@@ -494,7 +639,7 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
       __builtin_amdgcn_sched_barrier(0);
       // (5) dK^T += Q^T dS
       static_for<NT>([&](auto dt) {
-        static_for<2>([&](auto c) { dka[dt] = mfma32(tq[dt][c], db16[c], dka[dt]); });
+        static_for<2>([&](auto c) { dka[dt] = mfma32h(tq[dt][c], db16[c], dka[dt]); });
       });
     };
 
@@ -558,18 +703,18 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
             static_for<2>([&](auto e) {
               constexpr int r0 = 8 * hh + 4 * e;
               float4 a = dkp[e], bb = dvp[e];
-              a.x += dka[dt][r0 + 0] * scale; bb.x += dva[dt][r0 + 0];
-              a.y += dka[dt][r0 + 1] * scale; bb.y += dva[dt][r0 + 1];
-              a.z += dka[dt][r0 + 2] * scale; bb.z += dva[dt][r0 + 2];
-              a.w += dka[dt][r0 + 3] * scale; bb.w += dva[dt][r0 + 3];
+              a.x += dka[dt][r0 + 0] * dk_mul; bb.x += dva[dt][r0 + 0] * dv_mul;
+              a.y += dka[dt][r0 + 1] * dk_mul; bb.y += dva[dt][r0 + 1] * dv_mul;
+              a.z += dka[dt][r0 + 2] * dk_mul; bb.z += dva[dt][r0 + 2] * dv_mul;
+              a.w += dka[dt][r0 + 3] * dk_mul; bb.w += dva[dt][r0 + 3] * dv_mul;
               dkp[e] = a;
               dvp[e] = bb;
             });
           } else {
             bf16x8 a, bb;
             static_for<8>([&](auto i) {
-              a[int(i)] = static_cast<bf16>(dka[dt][8 * hh + i] * scale);
-              bb[int(i)] = static_cast<bf16>(dva[dt][8 * hh + i]);
+              a[int(i)] = static_cast<bf16>(dka[dt][8 * hh + i] * dk_mul);
+              bb[int(i)] = static_cast<bf16>(dva[dt][8 * hh + i] * dv_mul);
             });
             *reinterpret_cast<bf16x8 *>(static_cast<bf16 *>(dk_out) + off) = a;
             *reinterpret_cast<bf16x8 *>(static_cast<bf16 *>(dv_out) + off) = bb;
@@ -595,9 +740,13 @@ BwdLayout bwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, i
   L.gmask = align256b(L.ext + (size_t)n * sizeof(int32_t));
   L.items = align256b(L.gmask + (size_t)n * sizeof(unsigned long long));
   L.qitems = align256b(L.items + (size_t)L.max_items * sizeof(BwdItem));
-  L.stats = align256b(L.qitems + (size_t)L.max_qitems * sizeof(FwdItem));
+  L.q16 = align256b(L.qitems + (size_t)L.max_qitems * sizeof(FwdItem));
+  L.do16 = align256b(L.q16 + (size_t)n_q * h_q * d * sizeof(f16));
+  L.k16 = align256b(L.do16 + (size_t)n_q * h_q * d * sizeof(f16));
+  L.v16 = align256b(L.k16 + (size_t)n_kv * h_kv * d * sizeof(f16));
+  L.stats = align256b(L.v16 + (size_t)n_kv * h_kv * d * sizeof(f16));
   L.aug = align256b(L.stats + (size_t)h_q * L.nq_pad * 2 * sizeof(float));
-  L.total = align256b(L.aug + (size_t)h_q * (L.nq_pad / kRows) * kAugEl * sizeof(bf16));
+  L.total = align256b(L.aug + (size_t)h_q * (L.nq_pad / kRows) * kAugEl * sizeof(f16));
   return L;
 }
 
@@ -613,8 +762,12 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
   auto *gmask = reinterpret_cast<unsigned long long *>(ws + L.gmask);
   BwdItem *items = reinterpret_cast<BwdItem *>(ws + L.items);
   FwdItem *qitems = reinterpret_cast<FwdItem *>(ws + L.qitems);
+  f16 *q16 = reinterpret_cast<f16 *>(ws + L.q16);
+  f16 *do16 = reinterpret_cast<f16 *>(ws + L.do16);
+  f16 *k16 = reinterpret_cast<f16 *>(ws + L.k16);
+  f16 *v16 = reinterpret_cast<f16 *>(ws + L.v16);
   float *stats = reinterpret_cast<float *>(ws + L.stats);
-  bf16 *aug = reinterpret_cast<bf16 *>(ws + L.aug);
+  f16 *aug = reinterpret_cast<f16 *>(ws + L.aug);
   static bool attr_set = false;
   if (!attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_bwd_dkdv_kernel<D>),
@@ -632,7 +785,8 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
   if (T > 0) {
     hipLaunchKernelGGL(prep_bwd_kernel, dim3(1), dim3(kPrepThreads), 0, st, cu, n, tiles, T, h_q,
                        h_kv, n_q, n_kv, hdr, ext, gmask, items, L.max_items);
-    enqueue_fwd_items(cu, n, tiles, T, h_q, h_kv, n_q, n_kv, hdr, qitems, L.max_qitems, st);
+    enqueue_fwd_items(cu, n, tiles, T, h_q, h_kv, n_q, n_kv, hdr, qitems, L.max_qitems, false,
+                      st);
     {
       // stats and aug of rows outside the covered ones stay zero (finite):
       // they are only read for masked rows; lanes 32..63 of aug stay zero
@@ -640,19 +794,27 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
       hipLaunchKernelGGL(zero_kernel, dim3((unsigned)std::min<int64_t>((s16 + 255) / 256, 4096)),
                          dim3(256), 0, st, reinterpret_cast<uint4 *>(stats), s16);
     }
-    hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)(T * kTileSplit)), dim3(256), 0, st, o,
-                       dout, lse, tiles, h_q, n_q, n_kv, L.nq_pad, scale, stats, aug);
     int dev = 0, cus = 256;
     hipGetDevice(&dev);
     hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    hipLaunchKernelGGL(bwd_absmax_q_kernel<D>, dim3((unsigned)(T * kTileSplit)), dim3(256), 0, st,
+                       q, dout, tiles, h_q, n_q, n_kv, hdr, q16, do16);
+    hipLaunchKernelGGL((bwd_kv_pass_kernel<D, false>), dim3((unsigned)cus * 8), dim3(256), 0, st,
+                       k, v, cu, n, ext, h_kv, n_kv, hdr, k16, v16);
+    hipLaunchKernelGGL((bwd_kv_pass_kernel<D, true>), dim3((unsigned)cus * 8), dim3(256), 0, st,
+                       k, v, cu, n, ext, h_kv, n_kv, hdr, k16, v16);
+    hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)(T * kTileSplit)), dim3(256), 0, st, q,
+                       o, dout, lse, tiles, h_q, n_q, n_kv, L.nq_pad, scale, hdr, q16, do16,
+                       stats, aug);
+    // dQ first: it writes the -D records the dK / dV kernel reads
+    const int rc = launch_bwd_dq(D, q, dout, k, v, stats, cu, qitems, hdr, h_q, h_kv, n_q, n_kv,
+                                 L.nq_pad, scale, dq, aug, cus, st, tm_q);
+    if (rc != LIBRA_OK) return rc;
     if (tm_kv) hipEventRecord(tm_kv->begin, st);
-    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(cus), dim3(kThreads), KvShape<D>::SMEM, st, k,
-                       v, q, dout, aug, cu, tiles, T, items, hdr, h_q, h_kv, n_q, n_kv,
+    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(cus), dim3(kThreads), KvShape<D>::SMEM, st,
+                       k16, v16, q16, do16, aug, cu, tiles, T, items, hdr, h_q, h_kv, n_q, n_kv,
                        L.nq_pad, scale, scale * kLog2e, dk, dv, accumulate ? 1 : 0);
     if (tm_kv) hipEventRecord(tm_kv->end, st);
-    const int rc = launch_bwd_dq(D, q, dout, k, v, stats, cu, qitems, hdr, h_q, h_kv, n_q, n_kv,
-                                 L.nq_pad, scale, dq, cus, st, tm_q);
-    if (rc != LIBRA_OK) return rc;
   }
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(LIBRA_EHIP, "backward launch failed: %s", hipGetErrorString(e));

@@ -1,9 +1,18 @@
 // dQ kernel of the backward pass (gfx950): query-stationary and shaped like the
 // forward; its work items are the forward's.  Per 64-key block it recomputes
-// S^T = K Q^T and dP^T = V dO^T (lane = query), forms
+// S^T = K Q^T and dP^T - D = [V | 1] [dO | -D]^T (lane = query; D enters as
+// one extra k-block, as in the dK / dV kernel), forms
 // dS^T = P^T * (dP^T - D) on the VALU and accumulates dQ^T += K^T dS^T, with
 // the key blocks staged in a 4-deep LDS ring.  The VALU work of one key block
 // overlaps the S^T / dP^T products of the next.
+//
+// It runs before the dK / dV kernel and hands it D: D = rowsum(dO * O) equals
+// sum_k P_k dP_k (O = sum_k P_k V_k), which this kernel has in fp32 for every
+// key of the row, while the pre-pass can only form it from the bf16-rounded
+// O.  Since sum_k P_k = 1, sum_k dS_k = D_exact - D: the row sums of dS (per
+// key block, then over blocks) correct the pre-pass value, and replace the -D
+// record of the row in the dK / dV kernel's augmented operands; this kernel's
+// own dS uses the pre-pass value.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -31,13 +40,16 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
     const bf16 *__restrict__ v, const float *__restrict__ stats,
     const int64_t *__restrict__ cu, const FwdItem *__restrict__ items,
     int32_t *__restrict__ hdr, int h_q, int h_kv, int64_t n_q, int64_t n_kv, int64_t nq_pad,
-    float c2, float scale, bf16 *__restrict__ dq) {
+    float c2, float scale, bf16 *__restrict__ dq, f16 *__restrict__ aug) {
   using S = DqShape<D>;
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
   __shared__ int32_t s_item;
   const int tid = threadIdx.x, l = tid & 63, ln = l & 31, kg = l >> 5;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
   int q_serve = blockIdx.x % kXcds, q_left = kXcds;
+  // scale of -D in the dK / dV kernel's fp16 operands (s_o * s_v, fp16_scale)
+  const float s_ov = fp16_scale((uint32_t)hdr[kMaxAbs + 1], true) *
+                     fp16_scale((uint32_t)hdr[kMaxAbs + 3], true);
   // per-lane LDS offsets (elements): K / V rows perm32(ln) for S^T and dP^T,
   // and the transpose reads of the K tile that give the K^T operand of dQ^T
   // (as in the dK/dV kernel, with keys in place of query rows)
@@ -63,6 +75,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
     const int r = kst(u);
     k_lane[u] = 2u * (uint32_t)(r * h_kv * D + 8 * swt<S::KC>(r, l % S::KC));
   });
+  // A operand of the augmented k-block of dP^T: ones in k = 0, 1, 2
+  bf16x8 ones3;
+  static_for<8>([&](auto i) { ones3[int(i)] = bf16(kg == 0 && i < 3 ? 1.f : 0.f); });
 
   for (;;) {
     if (tid == 0) s_item = take_item(hdr, kFwdQ, q_serve, q_left);
@@ -95,6 +110,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
       l2 = st[row % kRows];
       dd_q = st[kRows + row % kRows];
     }
+    // -D as the B operand of dP^T's augmented k-block: [V | 1] [dO | -D]^T
+    bf16x8 dneg;
+    split3(kg == 0 ? -dd_q : 0.f, dneg);
 
     wait_vm_known();
     f32x16 acc[D / 32];
@@ -137,7 +155,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
     auto sdp = [&](int b, Acc2 &s, Acc2 &dp) {
       const bf16 *Ks = stage(b), *Vs = Ks + S::K_EL;
       static_for<2>([&](auto t) {
-        static_for<16>([&](auto r) { s[t][int(r)] = 0.f; dp[t][int(r)] = 0.f; });
+        static_for<16>([&](auto r) { s[t][int(r)] = 0.f; });
+        dp[t] = mfma32(ones3, dneg, mfma_zero_c());
         static_for<D / 16>([&](auto c) {
           s[t] = mfma32(*reinterpret_cast<const bf16x8 *>(Ks + 32 * t * D + koff[c]), qf[c], s[t]);
           dp[t] = mfma32(*reinterpret_cast<const bf16x8 *>(Vs + 32 * t * D + koff[c]), of[c],
@@ -145,20 +164,21 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
         });
       });
     };
-    // One element of dS^T = P^T * (dP^T - D) of the block in (s, dp):
+    // One element of dS^T = P^T * (dP^T - D) of the block in (s, dp), the
+    // products having subtracted D already:
     // register r of tile t, with P^T = exp2(S^T c2 - LSE log2 e); with MASK,
     // keys after the lane's query give P = 0
     const float neg_l2 = -l2;
     auto ds_elem = [&](auto mask_t, auto t, auto r, int b, Acc2 &s, Acc2 &dp,
-                       bf16x8 (&dsf)[4]) {
+                       bf16x8 (&dsf)[4], float &pdp) {
       float x = __builtin_fmaf(s[t][int(r)], c2, neg_l2);
       if constexpr (decltype(mask_t)::value) {
         const int kl = b * kFwdBN + 32 * t + 16 * (r >> 3) + 8 * kg + (r & 7);
         x = kl > qloc ? -INFINITY : x;
       }
-      const float p = fast_exp2(x);
-      const float d = dp[t][int(r)] - dd_q;
-      dsf[2 * t + (r >> 3)][r & 7] = static_cast<bf16>(p * d);
+      const float ds = fast_exp2(x) * dp[t][int(r)];
+      pdp += ds;
+      dsf[2 * t + (r >> 3)][r & 7] = static_cast<bf16>(ds);
     };
     // dQ^T += K^T dS^T of block b; key chunk c = 16 keys from tile row 16 c.
     // MFMA i = 4 dt + c; its transpose operand is read three MFMAs ahead.
@@ -182,7 +202,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
     // i = 2 NC t + 2 c + kind (kind 0: S^T from K, 1: dP^T from V); its K / V
     // operand is read four MFMAs ahead.
     auto phase_a = [&](auto mask_t, auto next_t, int b, Acc2 &sc, Acc2 &dc, Acc2 &sn, Acc2 &dn,
-                       bf16x8 (&dsf)[4]) {
+                       bf16x8 (&dsf)[4], float &pdp) {
       if constexpr (decltype(next_t)::value) {
         const bf16 *Ks = stage(b + 1), *Vs = Ks + S::K_EL;
         constexpr int NC = D / 16, NM = 4 * NC, AHEAD = 4;
@@ -199,24 +219,28 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
           constexpr int t = i / (2 * NC), c = (i % (2 * NC)) / 2, kind = i % 2;
           Acc2 &dst = kind ? dn : sn;
           const bf16x8 &bop = kind ? of[c] : qf[c];
-          dst[t] = mfma32(op[i], bop, c == 0 ? mfma_zero_c() : dst[t]);
+          if constexpr (c == 0 && kind == 1)
+            dst[t] = mfma32(op[i], bop, mfma32(ones3, dneg, mfma_zero_c()));
+          else
+            dst[t] = mfma32(op[i], bop, c == 0 ? mfma_zero_c() : dst[t]);
           if constexpr (i + AHEAD < NM) rd(std::integral_constant<int, i + AHEAD>{});
           static_for<EPM>([&](auto e) {
             constexpr int j = EPM * i + e;
             ds_elem(mask_t, std::integral_constant<int, j / 16>{},
-                    std::integral_constant<int, j % 16>{}, b, sc, dc, dsf);
+                    std::integral_constant<int, j % 16>{}, b, sc, dc, dsf, pdp);
           });
           __builtin_amdgcn_sched_barrier(0);
         });
       } else {
         static_for<2>([&](auto t) {
-          static_for<16>([&](auto r) { ds_elem(mask_t, t, r, b, sc, dc, dsf); });
+          static_for<16>([&](auto r) { ds_elem(mask_t, t, r, b, sc, dc, dsf, pdp); });
         });
       }
     };
 
     int issued = 0;
     for (; issued < nkb && issued < S::NSTAGE - 1; ++issued) issue(issued, issued);
+    float d_run = 0.f;   // this lane's half of sum_k dS_k over the row's keys
     auto iter = [&](int b, Acc2 &sc, Acc2 &dc, Acc2 &sn, Acc2 &dn) {
       if (b + 1 < nkb) {
         // block b + 1 landed (at most one later block in flight) and every
@@ -230,14 +254,16 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
       }
       if (b < wave_nkb) {
         bf16x8 dsf[4];
+        float pdp = 0.f;                                         // this block's sum of dS
         const bool mask = b * kFwdBN + kFwdBN - 1 > wave_qmin;   // reaches past the first row
         if (b + 1 < wave_nkb) {
-          if (mask) phase_a(std::true_type{}, std::true_type{}, b, sc, dc, sn, dn, dsf);
-          else phase_a(std::false_type{}, std::true_type{}, b, sc, dc, sn, dn, dsf);
+          if (mask) phase_a(std::true_type{}, std::true_type{}, b, sc, dc, sn, dn, dsf, pdp);
+          else phase_a(std::false_type{}, std::true_type{}, b, sc, dc, sn, dn, dsf, pdp);
         } else {
-          if (mask) phase_a(std::true_type{}, std::false_type{}, b, sc, dc, sn, dn, dsf);
-          else phase_a(std::false_type{}, std::false_type{}, b, sc, dc, sn, dn, dsf);
+          if (mask) phase_a(std::true_type{}, std::false_type{}, b, sc, dc, sn, dn, dsf, pdp);
+          else phase_a(std::false_type{}, std::false_type{}, b, sc, dc, sn, dn, dsf, pdp);
         }
+        d_run += pdp;
         dqm(b, dsf);
       }
     };
@@ -257,6 +283,14 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
     wait_vm_n<0>();
     __syncthreads();   // the ring is reused by the next item
 
+    // D_exact = D + sum_k dS_k (sum_k P_k = 1)
+    const float d_exact = dd_q + row_sum2(d_run);
+    if (active && ln < wrows && kg == 0) {
+      f16x8 rec;
+      split3h(-d_exact * s_ov, rec);
+      *reinterpret_cast<f16x8 *>(aug + ((size_t)head * (nq_pad / kRows) + row / kRows) * kAugEl +
+                                 kAugEl / 2 + 8 * perm32((int)(row % kRows))) = rec;
+    }
     if (active && ln < wrows) {
       bf16 *op = dq + ((size_t)row * h_q + head) * D + 8 * kg;
 #pragma unroll
@@ -275,7 +309,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
 int launch_bwd_dq(int d, const bf16 *q, const bf16 *dout, const bf16 *k, const bf16 *v,
                   const float *stats, const int64_t *cu, const FwdItem *items, int32_t *hdr,
                   int h_q, int h_kv, int64_t n_q, int64_t n_kv, int64_t nq_pad, float scale,
-                  bf16 *dq, int blocks, hipStream_t st, const KernelTimer *tm) {
+                  bf16 *dq, f16 *aug, int blocks, hipStream_t st, const KernelTimer *tm) {
   static bool attr_set[2] = {false, false};
   const int which = d == 128 ? 1 : 0;
   const void *fn = d == 128 ? reinterpret_cast<const void *>(&attn_bwd_dq_kernel<128>)
@@ -291,11 +325,11 @@ int launch_bwd_dq(int d, const bf16 *q, const bf16 *dout, const bf16 *k, const b
   if (d == 128)
     hipLaunchKernelGGL(attn_bwd_dq_kernel<128>, dim3(blocks), dim3(kThreads), smem, st, q, dout,
                        k, v, stats, cu, items, hdr, h_q, h_kv, n_q, n_kv, nq_pad, scale * kLog2e,
-                       scale, dq);
+                       scale, dq, aug);
   else
     hipLaunchKernelGGL(attn_bwd_dq_kernel<64>, dim3(blocks), dim3(kThreads), smem, st, q, dout,
                        k, v, stats, cu, items, hdr, h_q, h_kv, n_q, n_kv, nq_pad, scale * kLog2e,
-                       scale, dq);
+                       scale, dq, aug);
   if (tm) hipEventRecord(tm->end, st);
   return LIBRA_OK;
 }

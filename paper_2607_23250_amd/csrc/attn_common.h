@@ -16,6 +16,8 @@ typedef bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16;
+typedef f16 f16x8 __attribute__((ext_vector_type(8)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -44,8 +46,10 @@ enum HdrSlot {
   kBadTiles = 4,   // tiles skipped because they were out of range (+1 on item overflow)
   kFwdQ = 8,       // forward / dQ work items
   kBwdQ = 32,      // dK/dV work items
+  kMaxAbs = 56,    // backward: max |x| (fp32 bits) of Q, dO, K, V in slots 56..59
   kHdrSlots = 64
 };
+static_assert(kBadTiles * 4 == LIBRA_WS_SKIPPED_OFFSET, "documented offset of the skip count");
 
 // Cost bucket, 0 = longest: exact below 512, then 32 units per bucket.
 __device__ __forceinline__ int cost_bucket(int64_t c) {
@@ -147,7 +151,31 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+__device__ __forceinline__ f32x16 mfma32h(f16x8 a, f16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Lanes l and l ^ 32 hold the two halves of a query's row: v_permlane32_swap
+// on two copies of x pairs them up in every lane (lanes 0-31 get
+// (x[l], x[l + 32]), lanes 32-63 (x[l - 32], x[l])) without a round trip
+// through LDS; max and sum of the pair are symmetric, so both lanes of a row
+// get the same bits.
+__device__ __forceinline__ float row_max2(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float row_sum2(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Backward "aug" records: per 32-row block and query head, two MFMA
+// A-operands of 64 lanes x 8 fp16 (-LSE / scale, then -D; see bwd_pre_kernel).
+constexpr int kAugEl = 2 * 64 * 8;
 
 
 // Swizzle of row-major Q / dO / K / V tiles that are read both by rows
@@ -181,6 +209,15 @@ __device__ __forceinline__ bf16x4 lds_tr16(const bf16 *p) {
 __device__ __forceinline__ bf16x8 lds_tr16x2(const bf16 *p0, const bf16 *p1) {
   const bf16x4 a = lds_tr16(p0), b = lds_tr16(p1);
   return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// The same two transpose reads for an fp16 tile.
+__device__ __forceinline__ f16x8 lds_tr16x2h(const f16 *p0, const f16 *p1) {
+  const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4 *)(p0));
+  const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4 *)(p1));
+  return __builtin_bit_cast(f16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
 // Asynchronous 16-byte global -> LDS copy by one wave: lane i's bytes land at
@@ -351,6 +388,31 @@ __device__ __forceinline__ void split3(float x, bf16x8 &r) {
   r[2] = c;
 }
 
+// The same split in fp16: hi + mid + lo carry about 33 significant bits.
+__device__ __forceinline__ void split3h(float x, f16x8 &r) {
+  const f16 a = static_cast<f16>(x);
+  const float x1 = x - static_cast<float>(a);
+  const f16 b = static_cast<f16>(x1);
+  const f16 c = static_cast<f16>(x1 - static_cast<float>(b));
+  static_for<8>([&](auto i) { r[int(i)] = f16(0.f); });
+  r[0] = a;
+  r[1] = b;
+  r[2] = c;
+}
+
+// Power-of-two scale of a tensor whose max |x| has fp32 bits `mx`, for its
+// fp16 copy.  Gradient-side operands (dO, V) are brought to max |x s| in
+// [1, 2), up or down; score-side operands (Q, K) only down, to max |x s| in
+// [4, 8), so that the augmented -LSE operand of the dK / dV kernel stays
+// inside the fp16 range.  A zero or non-finite max gives s = 1.
+__host__ __device__ __forceinline__ float fp16_scale(uint32_t mx, bool up) {
+  const int e = (int)((mx >> 23) & 0xff) - 127;   // floor(log2 max) for a normal max
+  if (mx == 0 || e == 128 || e == -127) return 1.f;
+  int k = up ? -e : (e > 2 ? -(e - 2) : 0);
+  k = k < -126 ? -126 : (k > 126 ? 126 : k);
+  return __builtin_bit_cast(float, (uint32_t)(k + 127) << 23);
+}
+
 // s_waitcnt vmcnt(N) for a compile-time N.
 template <int N>
 __device__ __forceinline__ void wait_vm_n() {
@@ -415,7 +477,8 @@ struct FwdLayout {
   int64_t max_items = 0;
 };
 struct BwdLayout {
-  size_t hdr = 0, ext = 0, gmask = 0, items = 0, qitems = 0, stats = 0, aug = 0, total = 0;
+  size_t hdr = 0, ext = 0, gmask = 0, items = 0, qitems = 0, q16 = 0, do16 = 0, k16 = 0,
+         v16 = 0, stats = 0, aug = 0, total = 0;
   int64_t max_items = 0, max_qitems = 0, nq_pad = 0;
 };
 
@@ -431,7 +494,7 @@ struct KernelTimer {
 // used by the dQ kernel.
 void enqueue_fwd_items(const int64_t *cu, int64_t n, const libra_tile_t *tiles, int64_t T,
                        int h_q, int h_kv, int64_t n_q, int64_t n_kv, int32_t *hdr,
-                       FwdItem *items, int64_t max_items, hipStream_t st);
+                       FwdItem *items, int64_t max_items, bool count_bad, hipStream_t st);
 int64_t fwd_max_items(int64_t T, int64_t n, int64_t n_q, int h_q, int h_kv);
 
 int launch_fwd(const void *q, const void *k, const void *v, const int64_t *cu, int64_t n,
@@ -443,7 +506,7 @@ int launch_fwd(const void *q, const void *k, const void *v, const int64_t *cu, i
 int launch_bwd_dq(int d, const bf16 *q, const bf16 *dout, const bf16 *k, const bf16 *v,
                   const float *stats, const int64_t *cu, const FwdItem *items, int32_t *hdr,
                   int h_q, int h_kv, int64_t n_q, int64_t n_kv, int64_t nq_pad, float scale,
-                  bf16 *dq, int blocks, hipStream_t st, const KernelTimer *tm);
+                  bf16 *dq, f16 *aug, int blocks, hipStream_t st, const KernelTimer *tm);
 int launch_bwd(const void *q, const void *k, const void *v, const void *o, const float *lse,
                const void *dout, const int64_t *cu, int64_t n, const libra_tile_t *tiles,
                int64_t T, int64_t n_q, int64_t n_kv, int h_q, int h_kv, int d, float scale,

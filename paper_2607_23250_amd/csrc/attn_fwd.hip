@@ -26,22 +26,6 @@
 
 namespace libra {
 
-// Lanes l and l ^ 32 hold the two halves of a query's row: v_permlane32_swap
-// on two copies of x pairs them up in every lane (lanes 0-31 get
-// (x[l], x[l + 32]), lanes 32-63 (x[l - 32], x[l])) without a round trip
-// through LDS; max and sum of the pair are symmetric, so both lanes of a row
-// get the same bits.
-__device__ __forceinline__ float row_max2(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
-                                                  false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float row_sum2(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
-                                                  false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
 // ---------------------------------------------------------------------------
 // Work items: every tile is split into sample fragments; every fragment into
 // items of (<= 4 heads of one KV group) x (32 * 4 / heads rows), starting at
@@ -80,11 +64,12 @@ __device__ void for_each_fwd_item_in(const libra_tile_t &t, int64_t wa, int64_t 
 
 // One workgroup: every tile's items, longest-first, one queue per XCD keyed
 // by (KV head, head chunk) so that an XCD streams few K/V sequences.  Tiles
-// outside the buffers are skipped and counted in hdr[kBadTiles].
+// outside the buffers are skipped, and counted in hdr[kBadTiles] when
+// `count_bad` is set (the backward counts them in its own preparation pass).
 __global__ __launch_bounds__(kPrepThreads) void prep_fwd_kernel(
     const int64_t *__restrict__ cu, int64_t n, const libra_tile_t *__restrict__ tiles, int64_t T,
     int h_q, int h_kv, int64_t n_q, int64_t n_kv, int32_t *__restrict__ hdr,
-    FwdItem *__restrict__ items, int64_t max_items) {
+    FwdItem *__restrict__ items, int64_t max_items, int count_bad) {
   __shared__ int32_t hist[kXcds * kQBuckets];
   __shared__ int32_t part[kPrepThreads];
   __shared__ unsigned long long s_wmax;
@@ -94,7 +79,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_fwd_kernel(
   const int keys = h_kv * chunks;
   const int R = keys >= kXcds ? 1 : kXcds / keys;    // queues per key
   if (tid == 0) {
-    hdr[kBadTiles] = 0;
+    if (count_bad) hdr[kBadTiles] = 0;
     s_wmax = 0;
   }
   __threadfence();
@@ -111,7 +96,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_fwd_kernel(
     const unsigned long long w = (unsigned long long)((tl.q_end - tl.q_begin + kRows - 1) / kRows);
     wm = w > wm ? w : wm;
   }
-  if (bad) atomicAdd(&hdr[kBadTiles], bad);
+  if (bad && count_bad) atomicAdd(&hdr[kBadTiles], bad);
   if (wm) atomicMax(&s_wmax, wm);
   __syncthreads();
   const int64_t wmax = (int64_t)s_wmax;
@@ -372,7 +357,7 @@ static int launch_fwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const int64
     attr_set = true;
   }
   hipLaunchKernelGGL(prep_fwd_kernel, dim3(1), dim3(kPrepThreads), 0, st, cu, n, tiles, T, h_q,
-                     h_kv, n_q, n_kv, hdr, items, L.max_items);
+                     h_kv, n_q, n_kv, hdr, items, L.max_items, 1);
   int dev = 0, cus = 256;
   hipGetDevice(&dev);
   hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
@@ -388,9 +373,9 @@ static int launch_fwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const int64
 
 void enqueue_fwd_items(const int64_t *cu, int64_t n, const libra_tile_t *tiles, int64_t T,
                        int h_q, int h_kv, int64_t n_q, int64_t n_kv, int32_t *hdr,
-                       FwdItem *items, int64_t max_items, hipStream_t st) {
+                       FwdItem *items, int64_t max_items, bool count_bad, hipStream_t st) {
   hipLaunchKernelGGL(prep_fwd_kernel, dim3(1), dim3(kPrepThreads), 0, st, cu, n, tiles, T, h_q,
-                     h_kv, n_q, n_kv, hdr, items, max_items);
+                     h_kv, n_q, n_kv, hdr, items, max_items, count_bad ? 1 : 0);
 }
 
 int launch_fwd(const void *q, const void *k, const void *v, const int64_t *cu, int64_t n,

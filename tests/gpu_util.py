@@ -1,4 +1,6 @@
 """Helpers shared by the GPU parity tests (not collected by pytest)."""
+import json
+import os
 import sys
 
 import numpy as np
@@ -46,15 +48,23 @@ def half_ulp_bf16(ref):
     return np.where(a > 0, 2.0 ** (e - 8), 0.0)
 
 
-def check(name, got, ref, tol=O_TOL, bf16_out=False, ref_bf16=None):
-    """max-abs and relative-L2 error against float64.
+def _log(record):
+    """Append one parity record (JSON) to the file named by LIBRA_PARITY_LOG, if set."""
+    path = os.environ.get("LIBRA_PARITY_LOG")
+    if not path:
+        return
+    record["test"] = os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0]
+    with open(path, "a") as f:
+        f.write(json.dumps(record) + "\n")
 
-    * bf16 outputs: the max-abs bound is applied on top of the output's own
-      rounding (half a bf16 ulp of the exact value), which no bf16 result
-      can avoid;
-    * ``ref_bf16`` (the same attention in plain bf16 PyTorch): the paper's
-      fidelity criterion (Sec. 6.7) -- errors within twice that reference's
-      -- relaxes each bound when the reference itself exceeds half of it.
+
+def check(name, got, ref, tol=O_TOL, bf16_out=False):
+    """max-abs and relative-L2 error against float64, at the fixed bounds
+    (max-abs <= 2e-2, relative L2 <= 1e-2 for O, dQ, dK, dV).
+
+    bf16 outputs: the max-abs bound applies to the error beyond the output's
+    own rounding (half a bf16 ulp of the exact value), which no bf16 result
+    can avoid.  fp32 outputs (accumulate-mode dK / dV) get no allowance.
     """
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
@@ -63,13 +73,14 @@ def check(name, got, ref, tol=O_TOL, bf16_out=False, ref_bf16=None):
     if bf16_out and got.size:
         excess = float((np.abs(got - ref) - half_ulp_bf16(ref)).max())
     t_ma, t_rl = tol
-    extra = ""
-    if ref_bf16 is not None:
-        b_ma, b_rl = errors(ref_bf16, ref)
-        t_ma, t_rl = max(t_ma, 2 * b_ma), max(t_rl, 2 * b_rl)
-        extra = f" [bf16 torch: max_abs={b_ma:.3e} rel_l2={b_rl:.3e}]"
-    say(f"  {name}: max_abs={ma:.3e} (beyond bf16 rounding {excess:.3e}) rel_l2={rl:.3e}{extra}")
-    assert np.isfinite(got).all(), f"{name}: non-finite"
+    finite = bool(np.isfinite(got).all())
+    ok = finite and excess <= t_ma and rl <= t_rl
+    ref_max = float(np.abs(ref).max()) if ref.size else 0.0
+    _log(dict(name=name, elements=int(got.size), bf16_out=bool(bf16_out), max_abs=ma,
+              excess=excess, rel_l2=rl, ref_max_abs=ref_max, bound=[t_ma, t_rl], ok=ok))
+    say(f"  {name}: max_abs={ma:.3e} (beyond bf16 rounding {excess:.3e}) rel_l2={rl:.3e} "
+        f"|ref|max={ref_max:.3e}")
+    assert finite, f"{name}: non-finite"
     assert excess <= t_ma and rl <= t_rl, \
         f"{name}: max_abs {ma:.3e} (excess {excess:.3e}) rel_l2 {rl:.3e} over {(t_ma, t_rl)}"
 

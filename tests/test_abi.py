@@ -75,3 +75,15 @@ def test_attention_entry_points_validate_before_touching_the_device():
     rc = L.libra_attn_fwd(fake, fake, fake, fake, 1, fake, 1, 10, 10, 2, 1, 64, 0.0, fake, fake,
                           ctypes.c_void_p(4096 + 8), 1 << 30, None)
     assert rc == pl.LIBRA_EINVAL
+
+
+def test_skipped_tiles_query_rejects_null_arguments():
+    """The documented route to the skipped-tile count validates its arguments
+    on the host (no device access for NULL pointers)."""
+    import ctypes as C
+    L = pl.lib()
+    n = C.c_int32(-7)
+    assert L.libra_attn_skipped_tiles(None, C.byref(n), None) == pl.LIBRA_EINVAL
+    assert L.libra_attn_skipped_tiles(C.c_void_p(256), None, None) == pl.LIBRA_EINVAL
+    assert n.value == -7
+    assert pl.LIBRA_WS_SKIPPED_OFFSET == 16

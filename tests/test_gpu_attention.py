@@ -1,22 +1,18 @@
 """GPU parity of libra_attn_fwd / libra_attn_bwd against the float64 oracle.
 
 Every case prints its name and sizes before touching the GPU.  Outputs are
-compared element by element: max-abs <= 2e-2 and relative L2 <= 1e-2 for O,
-dQ, dK, dV; max-abs <= 1e-3 for the log-sum-exp.  bf16 outputs meet the
-max-abs bound beyond their own storage rounding (half a bf16 ulp of the exact
-value, which reaches 3e-2 for |dV| >= 8 when many heads and queries are
-summed).  On the small random pools (very short samples, up to 16 query heads
-per KV head) the gradients may instead meet the paper's criterion (Sec. 6.7):
-at most twice the error of the same attention computed in plain bf16
-PyTorch, which itself reaches 2.5e-2 on dK there.
-"""
+compared element by element at fixed bounds: max-abs <= 2e-2 and relative
+L2 <= 1e-2 for O, dQ, dK, dV; max-abs <= 1e-3 for the log-sum-exp.  bf16
+outputs meet the max-abs bound beyond their own storage rounding (half a
+bf16 ulp of the exact value, which reaches 3e-2 for |dV| >= 8 when many
+heads and queries are summed); fp32 outputs (accumulate-mode dK / dV) get no
+allowance."""
 import numpy as np
 import pytest
 import torch
 
 import paper_2607_23250_amd as pl
 from oracle import attention as oa
-from oracle.bf16_reference import attention_bf16
 import workloads as wl
 from gpu_util import DEV, LSE_TOL, check, cu_dev, fwd, plan, say, to_np
 
@@ -61,17 +57,16 @@ def test_bwd_small_random(seed):
     dq, dk, dv = pl.libra_attn_bwd(qd, kd, vd, o, lse, dod, cu, td)
     torch.cuda.synchronize()
     dQ, dK, dV = oa.attention_bwd(q, k, v, do, w.lengths, w.q_positions())
-    _, bq, bk, bv = attention_bf16(q, k, v, do, w.lengths)
-    check("dQ", to_np(dq), dQ, bf16_out=True, ref_bf16=bq)
-    check("dK", to_np(dk), dK, bf16_out=True, ref_bf16=bk)
-    check("dV", to_np(dv), dV, bf16_out=True, ref_bf16=bv)
+    check("dQ", to_np(dq), dQ, bf16_out=True)
+    check("dK", to_np(dk), dK, bf16_out=True)
+    check("dV", to_np(dv), dV, bf16_out=True)
     # fp32 dK / dV of the same call in accumulate mode
     dk32 = torch.zeros(kd.shape, dtype=torch.float32, device=DEV)
     dv32 = torch.zeros_like(dk32)
     pl.libra_attn_bwd(qd, kd, vd, o, lse, dod, cu, td, dk=dk32, dv=dv32, accumulate=True)
     torch.cuda.synchronize()
-    check("dK fp32", to_np(dk32), dK, ref_bf16=bk)
-    check("dV fp32", to_np(dv32), dV, ref_bf16=bv)
+    check("dK fp32", to_np(dk32), dK)
+    check("dV fp32", to_np(dv32), dV)
 
 
 def test_fwd_config1_full():
@@ -194,10 +189,9 @@ def test_bwd_per_worker_accumulate(seed):
         pl.libra_attn_bwd(qd, kd, vd, o, lse, dod, cu, td, dq=dq, dk=dk, dv=dv, accumulate=True)
     torch.cuda.synchronize()
     dQ, dK, dV = oa.attention_bwd(q, k, v, do, w.lengths, w.q_positions())
-    _, bq, bk, bv = attention_bf16(q, k, v, do, w.lengths)
-    check("dQ", to_np(dq), dQ, bf16_out=True, ref_bf16=bq)
-    check("dK", to_np(dk), dK, ref_bf16=bk)
-    check("dV", to_np(dv), dV, ref_bf16=bv)
+    check("dQ", to_np(dq), dQ, bf16_out=True)
+    check("dK", to_np(dk), dK)
+    check("dV", to_np(dv), dV)
 
 
 def test_empty_tile_list():
@@ -224,9 +218,9 @@ def test_empty_tile_list():
 
 
 def test_out_of_range_tiles_are_skipped():
-    """Tiles outside the buffers are skipped on the device and counted in the
-    workspace header (int32 slot 4); the other tiles' results are bit-identical
-    to a call without them."""
+    """Tiles outside the buffers are skipped on the device and counted (read
+    back with libra_attn_skipped_tiles, the int32 at LIBRA_WS_SKIPPED_OFFSET);
+    the other tiles' results are bit-identical to a call without them."""
     w = wl.small_random(5)
     say(f"[out-of-range tiles] heads=({w.h_q},{w.h_kv}) d={w.d} rows={w.n_q_rows}")
     tiles, _ = plan(w)
@@ -251,8 +245,10 @@ def test_out_of_range_tiles_are_skipped():
         o, lse = pl.libra_attn_fwd(q, k, v, cu, td, workspace=wsf)
         dq, dk, dv = pl.libra_attn_bwd(q, k, v, o, lse, do, cu, td, workspace=wsb)
         torch.cuda.synchronize()
-        skipped = (int(wsf[16:20].cpu().view(torch.int32).item()),
-                   int(wsb[16:20].cpu().view(torch.int32).item()))
+        skipped = (pl.libra_attn_skipped_tiles(wsf), pl.libra_attn_skipped_tiles(wsb))
+        # the documented byte offset holds the same count
+        assert skipped == (int(wsf[16:20].cpu().view(torch.int32).item()),
+                           int(wsb[16:20].cpu().view(torch.int32).item()))
         outs.append(([to_np(x) for x in (o, lse, dq, dk, dv)], skipped))
     (ref, skip0), (got, skip1) = outs
     assert skip0 == (0, 0), skip0
@@ -299,9 +295,8 @@ def test_fwd_bwd_ragged_shuffled_tiles(seed):
     torch.cuda.synchronize()
     O, LSE = oa.attention_fwd(q, k, v, w.lengths, w.q_positions())
     dQ, dK, dV = oa.attention_bwd(q, k, v, do, w.lengths, w.q_positions())
-    _, bq, bk, bv = attention_bf16(q, k, v, do, w.lengths)
     check("O", to_np(o), O, bf16_out=True)
     check("LSE", to_np(lse), LSE, (LSE_TOL, 1e-4))
-    check("dQ", to_np(dq), dQ, bf16_out=True, ref_bf16=bq)
-    check("dK fp32", to_np(dk32), dK, ref_bf16=bk)
-    check("dV fp32", to_np(dv32), dV, ref_bf16=bv)
+    check("dQ", to_np(dq), dQ, bf16_out=True)
+    check("dK fp32", to_np(dk32), dK)
+    check("dV fp32", to_np(dv32), dV)

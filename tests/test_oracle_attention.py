@@ -202,16 +202,45 @@ def test_useful_pairs_equal_plan_cost(name):
     assert sum(t.cost for t in tiles) == w.h_q * oa.useful_pairs(w.lengths, w.q_positions())
 
 
-def test_bf16_reference_tracks_the_oracle():
-    """The bf16 PyTorch reference (used only for the paper's 2x error
-    allowance) computes the same attention, to bf16 accuracy, on a subset of
-    rows too."""
-    from oracle.bf16_reference import attention_bf16
-    w = wl.workload(wl.W_256K, scale=64)
-    q, k, v, do = wl.tensors(4, w.n_q_rows, w.n_kv_rows, w.h_q, w.h_kv, w.d)
+def test_dq_only_mode_matches_full_backward():
+    """dkdv=False only skips the dK / dV sums: dQ is bit-identical."""
+    w = wl.small_random(4)
+    q, k, v, do = wl.tensors(w.seed, w.n_q_rows, w.n_kv_rows, w.h_q, w.h_kv, w.d)
+    rows = np.arange(0, w.n_q_rows, 7)
+    dQ1, _, _ = oa.attention_bwd(q, k, v, do, w.lengths, w.q_positions(), rows=rows)
+    dQ2, dK2, dV2 = oa.attention_bwd(q, k, v, do, w.lengths, w.q_positions(), rows=rows,
+                                     dkdv=False)
+    np.testing.assert_array_equal(dQ1, dQ2)
+    assert not dK2.any() and not dV2.any()
+
+
+@pytest.mark.parametrize("name,scale", [(wl.W_256K, 64), (wl.W_1M, 256), (wl.W_32K, 16)])
+def test_zero_k_closed_forms_match_the_oracle(name, scale):
+    """The K = 0 closed forms used at full size on the GPU (prefix means,
+    reverse prefix sums of dO, suffix sums for dK) equal the oracle with K = 0,
+    on replicas with a CP share (rows missing between the head and tail
+    chunks) and on a whole pack."""
+    import closed_forms as cf
+    w = wl.workload(name, scale=scale)
+    q, k, v, do = wl.tensors(w.seed, w.n_q_rows, w.n_kv_rows, w.h_q, w.h_kv, w.d)
+    k = torch.zeros_like(k)
     pos = w.q_positions()
-    O, dQ, dK, dV = attention_bf16(q, k, v, do, w.lengths, pos)
-    O64, _ = oa.attention_fwd(q, k, v, w.lengths, pos)
-    dQ64, dK64, dV64 = oa.attention_bwd(q, k, v, do, w.lengths, pos)
-    for a, b in ((O, O64), (dQ, dQ64), (dK, dK64), (dV, dV64)):
-        assert np.linalg.norm(a - b) <= 2e-2 * np.linalg.norm(b)
+    O, LSE = oa.attention_fwd(q, k, v, w.lengths, pos)
+    dQ, dK, dV = oa.attention_bwd(q, k, v, do, w.lengths, pos)
+    G = w.h_q // w.h_kv
+    scale_sm = 1.0 / np.sqrt(w.d)
+    np.testing.assert_allclose(LSE, np.broadcast_to(
+        np.log(pos - np.concatenate([[0], np.cumsum(w.lengths)])[
+            np.searchsorted(np.cumsum(w.lengths), pos, side="right")] + 1.0), LSE.shape),
+        atol=1e-12)
+    np.testing.assert_allclose(dQ, 0.0, atol=1e-12)
+    q64, do64, v64 = (t.double().numpy() for t in (q, do, v))
+    for g in range(w.h_kv):
+        hs = slice(g * G, (g + 1) * G)
+        mean = cf.prefix_mean_v(v64[:, g], w.lengths, pos)
+        np.testing.assert_allclose(O[:, g * G], mean, atol=1e-12)
+        np.testing.assert_allclose(dV[:, g], cf.zero_k_dv(do64[:, hs], w.lengths, pos,
+                                                          w.n_kv_rows), atol=1e-10)
+        np.testing.assert_allclose(dK[:, g], cf.zero_k_dk(q64[:, hs], do64[:, hs], v64[:, g],
+                                                          w.lengths, pos, w.n_kv_rows, scale_sm,
+                                                          chunk=13), atol=1e-10)

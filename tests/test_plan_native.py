@@ -53,7 +53,7 @@ def test_workloads_meet_load_target(name):
     assert w.V * loads.max() / loads.sum() <= 1.05
 
 
-@pytest.mark.parametrize("seed", range(300))
+@pytest.mark.parametrize("seed", range(1000))
 def test_random_small_bit_exact(seed):
     w = wl.tiny_random(seed, max_packs=4, max_len=96)
     rng = np.random.default_rng(seed)
@@ -62,7 +62,7 @@ def test_random_small_bit_exact(seed):
     _same(_native(w, elem_bytes=eb, tau=tau), _oracle(w, elem_bytes=eb, tau=tau))
 
 
-@pytest.mark.parametrize("seed", range(40))
+@pytest.mark.parametrize("seed", range(200))
 def test_random_q_ranges_bit_exact(seed):
     w = wl.tiny_random(seed + 1000, max_packs=3, max_len=96)
     rng = np.random.default_rng(seed)
