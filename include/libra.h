@@ -203,6 +203,31 @@ int libra_attn_fwd(const void *q, const void *k, const void *v, const int64_t *c
 #define LIBRA_WS_SKIPPED_OFFSET 16
 int libra_attn_skipped_tiles(const void *workspace, int32_t *count, void *stream);
 
+/*
+ * libra_attn_fwd_noalloc -- libra_attn_fwd without a workspace argument, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation).  Same arguments,
+ * semantics and errors as libra_attn_fwd, with the same kernels; the work
+ * items live in a device array built into the library, of
+ * LIBRA_FWD_NOALLOC_MAX_WORKSPACE bytes, one per device, held until the
+ * process ends.  The call allocates nothing and frees nothing (its first
+ * call on a device looks up that device's array).
+ *   Sizes whose libra_attn_workspace_size(..., 0) exceeds the array are
+ *   rejected with LIBRA_ENOSPC before anything is enqueued (16 MiB covers,
+ *   e.g., 65536 query rows x 32 heads of a 1M-token pack).
+ *   Every call on one device shares that device's array: calls that overlap
+ *   in time on one device (different streams, or host threads) race and
+ *   must be serialized by the caller.  Each call's preparation pass rewrites
+ *   every part of the array it later reads, so nothing needs clearing
+ *   between calls.  The skipped-tile count of these calls is not exposed.
+ */
+#define LIBRA_FWD_NOALLOC_MAX_WORKSPACE ((size_t)16 << 20)
+int libra_attn_fwd_noalloc(const void *q, const void *k, const void *v,
+                           const int64_t *cu_seqlens, int64_t num_samples,
+                           const libra_tile_t *tiles, int64_t num_tiles, int64_t n_q_rows,
+                           int64_t n_kv_rows, int32_t h_q, int32_t h_kv, int32_t head_dim,
+                           float softmax_scale, void *o, float *lse, void *stream);
+
 /* libra_attn_bwd flags */
 #define LIBRA_BWD_ACCUMULATE_DKV 1u /* dk, dv are fp32 and are added to (not overwritten) */
 

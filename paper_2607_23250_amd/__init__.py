@@ -34,8 +34,9 @@ assert TILE_DTYPE.itemsize == 56
 EXPORTED = ("libra_strerror", "libra_last_error", "libra_plan", "libra_vrsp",
             "libra_attn_workspace_size", "libra_attn_fwd", "libra_attn_bwd",
             "libra_timing_enable", "libra_timing_read", "libra_mfma_loop_size",
-            "libra_mfma_loop", "libra_attn_skipped_tiles")
+            "libra_mfma_loop", "libra_attn_skipped_tiles", "libra_attn_fwd_noalloc")
 LIBRA_WS_SKIPPED_OFFSET = 16
+LIBRA_FWD_NOALLOC_MAX_WORKSPACE = 16 << 20
 
 
 class LibraError(RuntimeError):
@@ -89,6 +90,9 @@ def lib() -> ctypes.CDLL:
                                        ctypes.POINTER(ctypes.c_int64)]
     L.libra_mfma_loop.restype = ctypes.c_int
     L.libra_mfma_loop.argtypes = [I32, I32, P, I64, P]
+    L.libra_attn_fwd_noalloc.restype = ctypes.c_int
+    L.libra_attn_fwd_noalloc.argtypes = [P, P, P, P, I64, P, I64, I64, I64, I32, I32, I32,
+                                         ctypes.c_float, P, P, P]
     L.libra_attn_skipped_tiles.restype = ctypes.c_int
     L.libra_attn_skipped_tiles.argtypes = [P, ctypes.POINTER(ctypes.c_int32), P]
     _lib = L

@@ -4,6 +4,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 #include <vector>
 
 #include "attn_common.h"
@@ -12,7 +13,36 @@
 
 using namespace libra;
 
+// Device scratch of libra_attn_fwd_noalloc: the forward's work-item
+// workspace, one copy per device (each GPU the library runs on holds it until
+// the process ends).  In host code `scratch` names a host-side stand-in: its
+// device address comes from hipGetSymbolAddress, per device (scratch_ptr).
+constexpr size_t kNoAllocScratchBytes = size_t(16) << 20;
+static_assert(kNoAllocScratchBytes == LIBRA_FWD_NOALLOC_MAX_WORKSPACE, "documented limit");
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device, looked up once per device.
+int scratch_ptr(void **out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(LIBRA_EHIP, "hipGetDevice failed");
+  if (dev < 0 || dev >= kMaxDevices) return fail(LIBRA_EUNSUPPORTED, "device index %d", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(LIBRA_EHIP, "hipGetSymbolAddress(scratch) failed: %s", hipGetErrorString(e));
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return LIBRA_OK;
+}
 
 constexpr int64_t kMaxRows = (int64_t(1) << 31) - 256;
 
@@ -125,6 +155,34 @@ extern "C" int libra_attn_fwd(const void *q, const void *k, const void *v,
   return launch_fwd(q, k, v, cu_seqlens, num_samples, tiles, num_tiles, n_q_rows, n_kv_rows, h_q,
                     h_kv, head_dim, scale, o, lse, workspace, L,
                     static_cast<hipStream_t>(stream), tm);
+}
+
+extern "C" int libra_attn_fwd_noalloc(const void *q, const void *k, const void *v,
+                                      const int64_t *cu_seqlens, int64_t num_samples,
+                                      const libra_tile_t *tiles, int64_t num_tiles,
+                                      int64_t n_q_rows, int64_t n_kv_rows, int32_t h_q,
+                                      int32_t h_kv, int32_t head_dim, float softmax_scale,
+                                      void *o, float *lse, void *stream) {
+  last_error_text().clear();
+  if (int rc = check_sizes(num_samples, n_q_rows, n_kv_rows, h_q, h_kv, head_dim)) return rc;
+  if (num_tiles < 0) return fail(LIBRA_EINVAL, "num_tiles < 0");
+  if (num_tiles == 0) return LIBRA_OK;
+  if (!q || !k || !v || !cu_seqlens || !tiles || !o || !lse)
+    return fail(LIBRA_EINVAL, "NULL tensor argument");
+  const FwdLayout L =
+      fwd_layout(num_tiles, num_samples, n_q_rows, n_kv_rows, h_q, h_kv, head_dim);
+  if (L.total > kNoAllocScratchBytes)
+    return fail(LIBRA_ENOSPC, "these sizes need %zu bytes of workspace, more than the %zu of "
+                "the built-in scratch; use libra_attn_fwd with a workspace",
+                L.total, kNoAllocScratchBytes);
+  void *ws = nullptr;
+  if (int rc = scratch_ptr(&ws)) return rc;
+  const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt((float)head_dim);
+  int rc = LIBRA_OK;
+  const KernelTimer *tm = next_timer(0, &rc);
+  if (rc) return rc;
+  return launch_fwd(q, k, v, cu_seqlens, num_samples, tiles, num_tiles, n_q_rows, n_kv_rows, h_q,
+                    h_kv, head_dim, scale, o, lse, ws, L, static_cast<hipStream_t>(stream), tm);
 }
 
 extern "C" int libra_attn_skipped_tiles(const void *workspace, int32_t *count, void *stream) {

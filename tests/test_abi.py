@@ -87,3 +87,22 @@ def test_skipped_tiles_query_rejects_null_arguments():
     assert L.libra_attn_skipped_tiles(C.c_void_p(256), None, None) == pl.LIBRA_EINVAL
     assert n.value == -7
     assert pl.LIBRA_WS_SKIPPED_OFFSET == 16
+
+
+def test_noalloc_forward_rejects_oversize_on_the_host():
+    """libra_attn_fwd_noalloc checks its sizes against the built-in scratch
+    before touching the device: a tile count whose work items exceed it is
+    LIBRA_ENOSPC (pointers are never dereferenced on the host)."""
+    import ctypes as C
+    L = pl.lib()
+    dummy = C.c_void_p(256)
+    T = pl.LIBRA_FWD_NOALLOC_MAX_WORKSPACE // 32
+    assert pl.libra_attn_workspace_size(T, 4, 4096, 4096, 8, 2, 128, False) > \
+        pl.LIBRA_FWD_NOALLOC_MAX_WORKSPACE
+    rc = L.libra_attn_fwd_noalloc(dummy, dummy, dummy, dummy, 4, dummy, T, 4096, 4096, 8, 2, 128,
+                                  C.c_float(0.0), dummy, dummy, None)
+    assert rc == pl.LIBRA_ENOSPC
+    assert b"built-in scratch" in L.libra_last_error()
+    rc = L.libra_attn_fwd_noalloc(dummy, dummy, dummy, dummy, 4, dummy, 16, 4096, 4096, 8, 2, 96,
+                                  C.c_float(0.0), dummy, dummy, None)
+    assert rc == pl.LIBRA_EUNSUPPORTED
