@@ -3,7 +3,7 @@
 // dP^T - D = [V | 1] [dO | -D]^T (lane = query; D enters as one extra
 // k-block, as in the dK / dV kernel), forms dS^T = P^T * (dP^T - D) on the
 // VALU and accumulates dQ^T += K^T dS^T, with the key blocks staged in a
-// 3-deep LDS ring.  Producer and consumer waves split this work (see the
+// 4-deep LDS ring.  Producer and consumer waves split this work (see the
 // kernel).
 //
 // It runs before the dK / dV kernel and hands it D: D = rowsum(dO * O) equals
@@ -27,10 +27,11 @@ struct DqShape {
   static constexpr int KC = D / 8;            // 16-byte columns of a K / V row
   static constexpr int K_EL = kFwdBN * D;
   static constexpr int STAGE = 2 * K_EL;      // K and V rows of one key block
-  static constexpr int NSTAGE = 3;            // LDS ring of key blocks
+  static constexpr int NSTAGE = 4;            // LDS ring of key blocks
   static constexpr int DS_EL = 4 * 64 * 8;    // dS^T of one slice and block (4 KiB)
   static constexpr int NSLOT = 2;             // dS^T hand-over slots per slice
   static constexpr int NK = kFwdBN * KC / 64 / kWaves;   // wave loads per K (V) tile
+  // at d = 128 the dynamic LDS is exactly the 160 KiB of a CU
   static constexpr size_t SMEM = (NSTAGE * STAGE + kWaves * NSLOT * DS_EL) * sizeof(bf16);
 };
 
@@ -41,8 +42,8 @@ struct DqShape {
 // K / V blocks and accumulates dQ^T += K^T dS^T one block behind.  While one
 // wave of a SIMD is on the VALU, the other keeps the matrix cores busy, and
 // the copies no longer stall the wave that does the VALU work.  One barrier
-// per block; the K / V ring has three stages (producers read block i while
-// consumers read block i - 1 and block i + 1 lands).
+// per block; the K / V ring has four stages (producers read block i while
+// consumers read block i - 1, and blocks i + 1 and i + 2 land).
 template <int D>
 __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
     const bf16 *__restrict__ q, const bf16 *__restrict__ dout, const bf16 *__restrict__ k,
@@ -52,7 +53,8 @@ __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
     float c2, float scale, bf16 *__restrict__ dq, f16 *__restrict__ aug) {
   using S = DqShape<D>;
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
-  __shared__ int32_t s_item;
+  // the item index lives in the first dS^T slot, free between items
+  int32_t &s_item = *reinterpret_cast<int32_t *>(smem + S::NSTAGE * S::STAGE);
   const int tid = threadIdx.x, l = tid & 63, ln = l & 31, kg = l >> 5;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
   const bool producer = wv < kWaves;
@@ -237,10 +239,13 @@ __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
       f32x16 acc[D / 32];
       static_for<D / 32>([&](auto dt) { acc[dt] = mfma_zero(); });
       if (nkb > 0) issue(0, k_lane);
+      if (nkb > 1) issue(1, k_lane);
       for (int i = 0; i <= nkb; ++i) {
-        wait_vm();        // this wave's copies of block i
+        // this wave's copies of block i (block i + 1's may stay in flight)
+        if (i + 1 < nkb) wait_vm_n<2 * S::NK>();
+        else wait_vm();
         barrier_nofence();
-        if (i + 1 < nkb) issue(i + 1, k_lane);
+        if (i + 2 < nkb) issue(i + 2, k_lane);
         const int b = i - 1;
         if (b >= 0 && b < wave_nkb) {
           const bf16 *Ks = smem + (b % S::NSTAGE) * S::STAGE;
