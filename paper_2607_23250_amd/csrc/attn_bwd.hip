@@ -439,7 +439,7 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
   const int G = h_q / h_kv;
   const int64_t nblk = nq_pad / kRows;
-  int q_serve = blockIdx.x % kXcds, q_left = kXcds;
+  int q_serve = xcd_of_workgroup(), q_left = kXcds;
   // per-lane LDS offsets (elements) of the operand reads: rows of Q / dO for
   // S and dP (row perm32(ln), 8 columns), and the transpose reads that give
   // dO^T / Q^T for dV^T and dK^T: this lane addresses 4 columns of row

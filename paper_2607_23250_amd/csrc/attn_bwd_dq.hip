@@ -59,6 +59,8 @@ __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
   const bool producer = wv < kWaves;
   const int w = wv & (kWaves - 1);                         // slice of the item
+  // the XCD under round-robin dispatch (the value xcd_of_workgroup() reads;
+  // this form gives this kernel the faster schedule)
   int q_serve = blockIdx.x % kXcds, q_left = kXcds;
   bf16 *ds_slots = smem + S::NSTAGE * S::STAGE + w * S::NSLOT * S::DS_EL;
   // scale of -D in the dK / dV kernel's fp16 operands (s_o * s_v, fp16_scale)

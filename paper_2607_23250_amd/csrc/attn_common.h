@@ -106,6 +106,13 @@ __device__ void build_queues(Each &&each, int32_t *hist, int32_t *part, int32_t 
   });
 }
 
+// The XCD this workgroup runs on, read from the hardware (XCC_ID, bits 3:0).
+// Workgroups are dispatched round-robin over the XCDs, so this equals
+// blockIdx.x % 8 on a device in single-partition mode.
+__device__ __forceinline__ int xcd_of_workgroup() {
+  return __builtin_amdgcn_s_getreg(20 | (3 << 11)) & (kXcds - 1);   // hwreg(XCC_ID, 0, 4)
+}
+
 // Thread 0 of a persistent workgroup: index of the next item to run, or -1.
 // `q` is the queue being served (starts at the workgroup's XCD), `left` the
 // number of queues not yet found empty.

@@ -139,7 +139,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
   __shared__ int32_t s_item;
   const int tid = threadIdx.x, l = tid & 63, ln = l & 31, kg = l >> 5;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
-  int q_serve = blockIdx.x % kXcds, q_left = kXcds;
+  int q_serve = xcd_of_workgroup(), q_left = kXcds;
   // per-lane LDS offsets (elements) of the operand reads, fixed for the kernel
   // K rows perm32(ln) for S^T; transpose reads of the V tile for the V^T
   // operand of O^T (rows = keys, as in the dQ kernel's K^T)
@@ -259,34 +259,42 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
             });
           });
         }
-        float mx = -INFINITY;
-        static_for<2>([&](auto t) {
-          static_for<16>([&](auto r) { mx = fmaxf(mx, s[t][int(r)]); });
-        });
-        mx = row_max2(mx) * c2;       // row max of the scaled scores (log2 units)
-        // Lazy rescaling: the running max only moves when the block max exceeds
-        // it by more than 8 (a factor 256 in P).  The decision is per row, so
-        // rows stay independent of each other; the wave skips the multiply
-        // when no row moves.
-        const bool move = mx > m_run + 8.f;
+        // P with the running max.  The block's row sum of P (needed anyway)
+        // bounds every P of the row, so the running max only has to move
+        // when that sum exceeds 256 (every P then stays <= 256, as with a
+        // max test); the first block always sets it.  Only then is the
+        // block's row max computed, the row rescaled and P recomputed.
+        bf16x8 pf[4];
+        float ps = 0.f;
+        auto expo = [&](float neg_m) {
+          ps = 0.f;
+          static_for<2>([&](auto t) {
+            static_for<16>([&](auto r) {
+              const float p = fast_exp2(__builtin_fmaf(s[t][int(r)], c2, neg_m));
+              ps += p;
+              pf[2 * t + (r >> 3)][r & 7] = static_cast<bf16>(p);
+            });
+          });
+        };
+        bool move = true;
+        if (b > 0) {
+          expo(-m_run);
+          move = !(row_sum2(ps) <= 256.f);
+        }
         if (__builtin_amdgcn_ballot_w64(move)) {
+          float mx = -INFINITY;
+          static_for<2>([&](auto t) {
+            static_for<16>([&](auto r) { mx = fmaxf(mx, s[t][int(r)]); });
+          });
+          mx = row_max2(mx) * c2;
           const float alpha = move ? fast_exp2(m_run - mx) : 1.f;
           m_run = move ? mx : m_run;
           l_run *= alpha;
           static_for<D / 32>([&](auto dt) {
             static_for<16>([&](auto r) { oacc[dt][int(r)] *= alpha; });
           });
+          expo(-m_run);
         }
-        bf16x8 pf[4];
-        float ps = 0.f;
-        const float neg_m = -m_run;
-        static_for<2>([&](auto t) {
-          static_for<16>([&](auto r) {
-            const float p = fast_exp2(__builtin_fmaf(s[t][int(r)], c2, neg_m));
-            ps += p;
-            pf[2 * t + (r >> 3)][r & 7] = static_cast<bf16>(p);
-          });
-        });
         l_run += ps;
         // O^T += V^T P^T; key chunk c = 16 keys from tile row 16 c
         static_for<D / 32>([&](auto dt) {
