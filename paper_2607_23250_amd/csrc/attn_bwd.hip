@@ -148,11 +148,33 @@ __global__ __launch_bounds__(kPrepThreads) void prep_bwd_kernel(
 // kMaxAbs + 0..3): Q and dO over the covered (row, head) pairs, K and V over
 // the keys of the dK / dV work items.
 
-// Wave-wide max of non-negative floats, then one atomic per wave.
-__device__ __forceinline__ void wave_max_to(float m, int32_t *slot) {
-  for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
-  if ((threadIdx.x & 63) == 0 && m > 0.f)
-    atomicMax(reinterpret_cast<unsigned int *>(slot), __float_as_uint(m));
+// Workgroup-wide max of two non-negative floats (256 threads), then at most
+// one atomic per slot and workgroup, skipped when the slot already holds as
+// much (fp32 bits of non-negative floats order like unsigned integers).  Per
+// wave atomics on the same two slots serialise: thousands of them took
+// longer than the pass's loads.
+__device__ __forceinline__ void block_max2_to(float a, float b, int32_t *slot_a,
+                                              int32_t *slot_b) {
+  __shared__ float red[2][4];
+  for (int o = 32; o > 0; o >>= 1) {
+    a = fmaxf(a, __shfl_xor(a, o));
+    b = fmaxf(b, __shfl_xor(b, o));
+  }
+  const int tid = threadIdx.x;
+  if ((tid & 63) == 0) {
+    red[0][tid >> 6] = a;
+    red[1][tid >> 6] = b;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    a = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3]));
+    b = fmaxf(fmaxf(red[1][0], red[1][1]), fmaxf(red[1][2], red[1][3]));
+    const unsigned ua = __float_as_uint(a), ub = __float_as_uint(b);
+    if (a > 0.f && ua > (unsigned)ld_agent(slot_a))
+      atomicMax(reinterpret_cast<unsigned int *>(slot_a), ua);
+    if (b > 0.f && ub > (unsigned)ld_agent(slot_b))
+      atomicMax(reinterpret_cast<unsigned int *>(slot_b), ub);
+  }
 }
 
 __device__ __forceinline__ float absmax8(const bf16x8 &x) {
@@ -198,8 +220,7 @@ __global__ __launch_bounds__(256) void bwd_absmax_q_kernel(
       });
     }
   }
-  wave_max_to(mq, &hdr[kMaxAbs + 0]);
-  wave_max_to(mo, &hdr[kMaxAbs + 1]);
+  block_max2_to(mq, mo, &hdr[kMaxAbs + 0], &hdr[kMaxAbs + 1]);
 }
 
 // The keys the dK / dV kernel loads: for every sample with covered rows,
@@ -250,8 +271,7 @@ __global__ __launch_bounds__(256) void bwd_kv_pass_kernel(
     }
   }
   if constexpr (!CONVERT) {
-    wave_max_to(mk, &hdr[kMaxAbs + 2]);
-    wave_max_to(mv, &hdr[kMaxAbs + 3]);
+    block_max2_to(mk, mv, &hdr[kMaxAbs + 2], &hdr[kMaxAbs + 3]);
   }
 }
 

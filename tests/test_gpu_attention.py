@@ -69,6 +69,43 @@ def test_bwd_small_random(seed):
     check("dV fp32", to_np(dv32), dV)
 
 
+# Inputs scaled by powers of two, with the score scale a * b = 1 so that S,
+# P and LSE are unchanged: O scales by c, dV by e, dQ by e c b, dK by e c a.
+# The rescaled outputs must match the oracle of the unscaled inputs.  These
+# exercise the backward's fp16 operand scaling in both directions (tiny dO
+# or V scaled up; large Q, K, V or dO scaled down).
+MAGNITUDES = [(0, 0, 0, -14), (0, 0, 0, 13), (0, 0, 12, 0), (0, 0, -12, 0),
+              (-6, 6, 0, 0), (5, -5, 0, 0), (4, -4, -8, 10)]
+
+
+@pytest.mark.parametrize("exps", MAGNITUDES, ids=lambda e: "q%d_k%d_v%d_do%d" % tuple(e))
+def test_bwd_input_magnitudes(exps):
+    a, b, c, e = (2.0 ** x for x in exps)
+    w = wl.small_random(3)
+    say(f"[bwd magnitudes q*{a:g} k*{b:g} v*{c:g} dO*{e:g}] packs={w.pack_tokens} "
+        f"heads=({w.h_q},{w.h_kv}) d={w.d}")
+    tiles, _ = plan(w)
+    q, k, v, do = _inputs(w)
+    qd, kd, vd, dod = _dev(q * a, k * b, v * c, do * e)
+    cu = cu_dev(w)
+    td = pl.tiles_to_device(tiles, DEV)
+    o, lse = pl.libra_attn_fwd(qd, kd, vd, cu, td)
+    dq, dk, dv = pl.libra_attn_bwd(qd, kd, vd, o, lse, dod, cu, td)
+    dk32 = torch.zeros(kd.shape, dtype=torch.float32, device=DEV)
+    dv32 = torch.zeros_like(dk32)
+    pl.libra_attn_bwd(qd, kd, vd, o, lse, dod, cu, td, dk=dk32, dv=dv32, accumulate=True)
+    torch.cuda.synchronize()
+    O, LSE = oa.attention_fwd(q, k, v, w.lengths, w.q_positions())
+    dQ, dK, dV = oa.attention_bwd(q, k, v, do, w.lengths, w.q_positions())
+    check("O", to_np(o) / c, O, bf16_out=True)
+    check("LSE", to_np(lse), LSE, (LSE_TOL, 1e-4))
+    check("dQ", to_np(dq) / (e * c * b), dQ, bf16_out=True)
+    check("dK", to_np(dk) / (e * c * a), dK, bf16_out=True)
+    check("dV", to_np(dv) / e, dV, bf16_out=True)
+    check("dK fp32", to_np(dk32) / (e * c * a), dK)
+    check("dV fp32", to_np(dv32) / e, dV)
+
+
 def test_fwd_config1_full():
     w = wl.workload(wl.W_4K)
     say(f"[fwd 4K] {w.name} samples={len(w.lengths)}")
