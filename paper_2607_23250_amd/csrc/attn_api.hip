@@ -169,8 +169,9 @@ extern "C" int libra_attn_fwd_noalloc(const void *q, const void *k, const void *
   if (num_tiles == 0) return LIBRA_OK;
   if (!q || !k || !v || !cu_seqlens || !tiles || !o || !lse)
     return fail(LIBRA_EINVAL, "NULL tensor argument");
+  // no split K here: its partial slots would not fit the scratch
   const FwdLayout L =
-      fwd_layout(num_tiles, num_samples, n_q_rows, n_kv_rows, h_q, h_kv, head_dim);
+      fwd_layout(num_tiles, num_samples, n_q_rows, n_kv_rows, h_q, h_kv, head_dim, false);
   if (L.total > kNoAllocScratchBytes)
     return fail(LIBRA_ENOSPC, "these sizes need %zu bytes of workspace, more than the %zu of "
                 "the built-in scratch; use libra_attn_fwd with a workspace",

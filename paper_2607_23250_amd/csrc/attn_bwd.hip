@@ -113,7 +113,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_bwd_kernel(
     f(BwdItem{(int32_t)j, kb, g, 0}, (int64_t)(e - kb * kBwdBK + kRows - 1) / kRows,
       (g * R + kb % R) % kXcds);
   };
-  auto each = [&](auto &&f) {
+  auto each = [&](auto &&f, bool) {
     for (int64_t j = tid; j < n; j += kPrepThreads) {
       const int32_t e = ld_agent(&ext[j]);
       if (e == 0) continue;
@@ -766,7 +766,10 @@ BwdLayout bwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, i
   L.v16 = align256b(L.k16 + (size_t)n_kv * h_kv * d * sizeof(f16));
   L.stats = align256b(L.v16 + (size_t)n_kv * h_kv * d * sizeof(f16));
   L.aug = align256b(L.stats + (size_t)h_q * L.nq_pad * 2 * sizeof(float));
-  L.total = align256b(L.aug + (size_t)h_q * (L.nq_pad / kRows) * kAugEl * sizeof(f16));
+  L.splits = align256b(L.aug + (size_t)h_q * (L.nq_pad / kRows) * kAugEl * sizeof(f16));
+  L.max_parts = kFwdSplitSlots;
+  L.parts = align256b(L.splits + (size_t)(L.max_parts / 2) * sizeof(FwdSplit));
+  L.total = align256b(L.parts + (size_t)L.max_parts * fwd_part_floats(d) * sizeof(float));
   return L;
 }
 
@@ -805,18 +808,22 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
   if (T > 0) {
     hipLaunchKernelGGL(prep_bwd_kernel, dim3(1), dim3(kPrepThreads), 0, st, cu, n, tiles, T, h_q,
                        h_kv, n_q, n_kv, hdr, ext, gmask, items, L.max_items);
-    enqueue_fwd_items(cu, n, tiles, T, h_q, h_kv, n_q, n_kv, hdr, qitems, L.max_qitems, false,
-                      st);
-    {
-      // stats and aug of rows outside the covered ones stay zero (finite):
-      // they are only read for masked rows; lanes 32..63 of aug stay zero
-      const int64_t s16 = (int64_t)(L.total - L.stats) / 16;
-      hipLaunchKernelGGL(zero_kernel, dim3((unsigned)std::min<int64_t>((s16 + 255) / 256, 4096)),
-                         dim3(256), 0, st, reinterpret_cast<uint4 *>(stats), s16);
-    }
     int dev = 0, cus = 256;
     hipGetDevice(&dev);
     hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    // the dQ kernel runs one workgroup per CU; its items split K like the
+    // forward's when there are few of them
+    auto *splits = reinterpret_cast<FwdSplit *>(ws + L.splits);
+    float *parts = reinterpret_cast<float *>(ws + L.parts);
+    enqueue_fwd_items(cu, n, tiles, T, h_q, h_kv, n_q, n_kv, hdr, qitems, L.max_qitems, false,
+                      cus, L.max_parts, splits, st);
+    {
+      // stats and aug of rows outside the covered ones stay zero (finite):
+      // they are only read for masked rows; lanes 32..63 of aug stay zero
+      const int64_t s16 = (int64_t)(L.splits - L.stats) / 16;
+      hipLaunchKernelGGL(zero_kernel, dim3((unsigned)std::min<int64_t>((s16 + 255) / 256, 4096)),
+                         dim3(256), 0, st, reinterpret_cast<uint4 *>(stats), s16);
+    }
     hipLaunchKernelGGL(bwd_absmax_q_kernel<D>, dim3((unsigned)(T * kTileSplit)), dim3(256), 0, st,
                        q, dout, tiles, h_q, n_q, n_kv, hdr, q16, do16);
     hipLaunchKernelGGL((bwd_kv_pass_kernel<D, false>), dim3((unsigned)cus * 8), dim3(256), 0, st,
@@ -828,7 +835,8 @@ static int launch_bwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 
                        stats, aug);
     // dQ first: it writes the -D records the dK / dV kernel reads
     const int rc = launch_bwd_dq(D, q, dout, k, v, stats, cu, qitems, hdr, h_q, h_kv, n_q, n_kv,
-                                 L.nq_pad, scale, dq, aug, cus, st, tm_q);
+                                 L.nq_pad, scale, dq, aug, splits, parts, L.max_parts, cus,
+                                 st, tm_q);
     if (rc != LIBRA_OK) return rc;
     if (tm_kv) hipEventRecord(tm_kv->begin, st);
     hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(cus), dim3(kThreads), KvShape<D>::SMEM, st,

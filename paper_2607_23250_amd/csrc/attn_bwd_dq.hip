@@ -50,7 +50,8 @@ __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
     const bf16 *__restrict__ v, const float *__restrict__ stats,
     const int64_t *__restrict__ cu, const FwdItem *__restrict__ items,
     int32_t *__restrict__ hdr, int h_q, int h_kv, int64_t n_q, int64_t n_kv, int64_t nq_pad,
-    float c2, float scale, bf16 *__restrict__ dq, f16 *__restrict__ aug) {
+    float c2, float scale, bf16 *__restrict__ dq, f16 *__restrict__ aug,
+    float *__restrict__ parts) {
   using S = DqShape<D>;
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
   // the item index lives in the first dS^T slot, free between items
@@ -90,7 +91,7 @@ __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
     const int64_t row = (int64_t)it.q_row0 + wrow0 + my_r;
     const int qloc = it.q_loc0 + wrow0 + my_r;
     const int wave_qmin = it.q_loc0 + wrow0;
-    const int nkb = (it.q_loc0 + it.nrows - 1) / kFwdBN + 1;
+    const int kb0 = it.kb0, nkb = it.kb1;   // key blocks [kb0, nkb)
     const int wave_nkb = active ? (it.q_loc0 + wrow0 + wrows - 1) / kFwdBN + 1 : 0;
 
     // global -> LDS (consumers), asynchronous: K and V rows of key block b
@@ -99,9 +100,9 @@ __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
     auto issue = [&](int b, const uint32_t (&k_lane)[S::NK]) {
       bf16 *Ks = smem + (b % S::NSTAGE) * S::STAGE;
       bf16 *Vs = Ks + S::K_EL;
-      const int64_t kb0 = key0 + (int64_t)b * kFwdBN;
-      if (kb0 + kFwdBN <= n_kv) {
-        const size_t off = ((size_t)kb0 * h_kv + it.g) * D;
+      const int64_t kbase = key0 + (int64_t)b * kFwdBN;
+      if (kbase + kFwdBN <= n_kv) {
+        const size_t off = ((size_t)kbase * h_kv + it.g) * D;
         const uint32_t lk = lds_addr(Ks) + 1024u * w, lv = lds_addr(Vs) + 1024u * w;
         static_for<S::NK / 2>([&](auto h) {
           constexpr uint32_t d0 = 2 * h * kWaves * 1024u, d1 = d0 + kWaves * 1024u;
@@ -198,7 +199,7 @@ __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
         return dsum;
       };
       float d_run = 0.f;   // this lane's half of sum_k dS_k over the row's keys
-      for (int i = 0; i <= nkb; ++i) {
+      for (int i = kb0; i <= nkb; ++i) {
         // block i landed for every wave; dS^T of block i - 1 is in its slot
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         barrier_nofence();
@@ -212,8 +213,14 @@ __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
       }
       // D_exact = D + sum_k dS_k (sum_k P_k = 1): the -D record of the dK / dV
       // kernel's augmented operands for this (row, head)
-      const float d_exact = dd_q + row_sum2(d_run);
-      if (active && ln < wrows && kg == 0) {
+      const float d_part = row_sum2(d_run);
+      const float d_exact = dd_q + d_part;
+      if (it.slot >= 0) {
+        // a part of a split item: its sum of dS, merged by bwd_dq_combine_kernel
+        if (active && ln < wrows && kg == 0)
+          parts[(size_t)it.slot * fwd_part_floats(D) + (size_t)kFwdPartRows * D + w * kRows + ln] =
+              d_part;
+      } else if (active && ln < wrows && kg == 0) {
         f16x8 rec;
         split3h(-d_exact * s_ov, rec);
         *reinterpret_cast<f16x8 *>(aug + ((size_t)head * (nq_pad / kRows) + row / kRows) * kAugEl +
@@ -240,16 +247,16 @@ __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
       });
       f32x16 acc[D / 32];
       static_for<D / 32>([&](auto dt) { acc[dt] = mfma_zero(); });
-      if (nkb > 0) issue(0, k_lane);
-      if (nkb > 1) issue(1, k_lane);
-      for (int i = 0; i <= nkb; ++i) {
+      if (kb0 < nkb) issue(kb0, k_lane);
+      if (kb0 + 1 < nkb) issue(kb0 + 1, k_lane);
+      for (int i = kb0; i <= nkb; ++i) {
         // this wave's copies of block i (block i + 1's may stay in flight)
         if (i + 1 < nkb) wait_vm_n<2 * S::NK>();
         else wait_vm();
         barrier_nofence();
         if (i + 2 < nkb) issue(i + 2, k_lane);
         const int b = i - 1;
-        if (b >= 0 && b < wave_nkb) {
+        if (b >= kb0 && b < wave_nkb) {
           const bf16 *Ks = smem + (b % S::NSTAGE) * S::STAGE;
           const bf16 *slot = ds_slots + (b & 1) * S::DS_EL;
           bf16x8 dsf[4];
@@ -272,7 +279,21 @@ __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
           });
         }
       }
-      if (active && ln < wrows) {
+      if (active && ln < wrows && it.slot >= 0) {
+        // a part of a split item: unscaled fp32 dQ into its partial slot
+        float *op = parts + (size_t)it.slot * fwd_part_floats(D) + (size_t)(w * kRows + ln) * D +
+                    8 * kg;
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            float4 *dst = reinterpret_cast<float4 *>(op + 32 * dt + 16 * hh);
+            dst[0] = make_float4(acc[dt][8 * hh], acc[dt][8 * hh + 1], acc[dt][8 * hh + 2],
+                                 acc[dt][8 * hh + 3]);
+            dst[1] = make_float4(acc[dt][8 * hh + 4], acc[dt][8 * hh + 5], acc[dt][8 * hh + 6],
+                                 acc[dt][8 * hh + 7]);
+          }
+      } else if (active && ln < wrows) {
         bf16 *op = dq + ((size_t)row * h_q + head) * D + 8 * kg;
 #pragma unroll
         for (int dt = 0; dt < D / 32; ++dt)
@@ -289,10 +310,70 @@ __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
   }
 }
 
+// Merges the parts of every split item (hdr[kFwdSplits] records): dQ is the
+// scaled sum of the parts' fp32 dQ; D_exact = D + the parts' sums of dS gives
+// the -D record of the dK / dV kernel, as the dQ kernel writes it for whole
+// items.  Two threads per row (half of the head dimension each).
+template <int D>
+__global__ __launch_bounds__(256) void bwd_dq_combine_kernel(
+    const FwdSplit *__restrict__ splits, const int32_t *__restrict__ hdr,
+    const float *__restrict__ parts, const float *__restrict__ stats, int h_q, int64_t nq_pad,
+    float scale, bf16 *__restrict__ dq, f16 *__restrict__ aug) {
+  constexpr size_t PF = fwd_part_floats(D);
+  const int count = hdr[kFwdSplits];
+  const float s_ov = fp16_scale((uint32_t)hdr[kMaxAbs + 1], true) *
+                     fp16_scale((uint32_t)hdr[kMaxAbs + 3], true);
+  const int tid = threadIdx.x, pr = tid >> 1, half = tid & 1;
+  const int w = pr >> 5, r = pr & 31;   // wave slice and row of the item
+  for (int e = blockIdx.x; e < count; e += gridDim.x) {
+    const FwdSplit sp = splits[e];
+    const FwdItem &it = sp.item;
+    const int wrow0 = (w / it.nh) * kRows;
+    const int wrows = min(max(it.nrows - wrow0, 0), kRows);
+    if (r >= wrows) continue;
+    const int head = it.head0 + (w % it.nh);
+    const int64_t row = (int64_t)it.q_row0 + wrow0 + r;
+    float acc[D / 2];
+#pragma unroll
+    for (int i = 0; i < D / 2; ++i) acc[i] = 0.f;
+    float dsum = 0.f;
+    for (int p = 0; p < sp.parts; ++p) {
+      const float *rec = parts + (size_t)(sp.base + p) * PF;
+      dsum += rec[(size_t)kFwdPartRows * D + pr];
+      const float4 *src = reinterpret_cast<const float4 *>(rec + (size_t)pr * D + half * (D / 2));
+#pragma unroll
+      for (int i = 0; i < D / 8; ++i) {
+        const float4 x = src[i];
+        acc[4 * i] += x.x;
+        acc[4 * i + 1] += x.y;
+        acc[4 * i + 2] += x.z;
+        acc[4 * i + 3] += x.w;
+      }
+    }
+    bf16 *op = dq + ((size_t)row * h_q + head) * D + half * (D / 2);
+#pragma unroll
+    for (int i = 0; i < D / 16; ++i) {
+      bf16x8 ov;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) ov[j] = static_cast<bf16>(acc[8 * i + j] * scale);
+      *reinterpret_cast<bf16x8 *>(op + 8 * i) = ov;
+    }
+    if (half == 0) {
+      const size_t blk = (size_t)head * (nq_pad / kRows) + row / kRows;
+      const float d_exact = stats[blk * 2 * kRows + kRows + row % kRows] + dsum;
+      f16x8 rec;
+      split3h(-d_exact * s_ov, rec);
+      *reinterpret_cast<f16x8 *>(aug + blk * kAugEl + kAugEl / 2 + 8 * perm32((int)(row % kRows))) =
+          rec;
+    }
+  }
+}
+
 int launch_bwd_dq(int d, const bf16 *q, const bf16 *dout, const bf16 *k, const bf16 *v,
                   const float *stats, const int64_t *cu, const FwdItem *items, int32_t *hdr,
                   int h_q, int h_kv, int64_t n_q, int64_t n_kv, int64_t nq_pad, float scale,
-                  bf16 *dq, f16 *aug, int blocks, hipStream_t st, const KernelTimer *tm) {
+                  bf16 *dq, f16 *aug, const FwdSplit *splits, float *parts, int max_parts,
+                  int blocks, hipStream_t st, const KernelTimer *tm) {
   static bool attr_set[2] = {false, false};
   const int which = d == 128 ? 1 : 0;
   const void *fn = d == 128 ? reinterpret_cast<const void *>(&attn_bwd_dq_kernel<128>)
@@ -305,14 +386,21 @@ int launch_bwd_dq(int d, const bf16 *q, const bf16 *dout, const bf16 *k, const b
     attr_set[which] = true;
   }
   if (tm) hipEventRecord(tm->begin, st);
-  if (d == 128)
+  if (d == 128) {
     hipLaunchKernelGGL(attn_bwd_dq_kernel<128>, dim3(blocks), dim3(2 * kThreads), smem, st, q, dout,
                        k, v, stats, cu, items, hdr, h_q, h_kv, n_q, n_kv, nq_pad, scale * kLog2e,
-                       scale, dq, aug);
-  else
+                       scale, dq, aug, parts);
+    if (max_parts > 0)
+      hipLaunchKernelGGL(bwd_dq_combine_kernel<128>, dim3(blocks), dim3(256), 0, st, splits, hdr,
+                         parts, stats, h_q, nq_pad, scale, dq, aug);
+  } else {
     hipLaunchKernelGGL(attn_bwd_dq_kernel<64>, dim3(blocks), dim3(2 * kThreads), smem, st, q, dout,
                        k, v, stats, cu, items, hdr, h_q, h_kv, n_q, n_kv, nq_pad, scale * kLog2e,
-                       scale, dq, aug);
+                       scale, dq, aug, parts);
+    if (max_parts > 0)
+      hipLaunchKernelGGL(bwd_dq_combine_kernel<64>, dim3(blocks), dim3(256), 0, st, splits, hdr,
+                         parts, stats, h_q, nq_pad, scale, dq, aug);
+  }
   if (tm) hipEventRecord(tm->end, st);
   return LIBRA_OK;
 }

@@ -47,6 +47,7 @@ enum HdrSlot {
   kFwdQ = 8,       // forward / dQ work items
   kBwdQ = 32,      // dK/dV work items
   kMaxAbs = 56,    // backward: max |x| (fp32 bits) of Q, dO, K, V in slots 56..59
+  kFwdSplits = 60, // forward: split items (FwdSplit records), then partial slots used (61)
   kHdrSlots = 64
 };
 static_assert(kBadTiles * 4 == LIBRA_WS_SKIPPED_OFFSET, "documented offset of the skip count");
@@ -58,8 +59,10 @@ __device__ __forceinline__ int cost_bucket(int64_t c) {
 }
 
 // One workgroup of kPrepThreads: counts items per (queue, bucket), scans, and
-// scatters them so that each queue's segment is longest-first.  `each(f)`
-// must call f(item, cost, queue) once per item, in the same way every time.
+// scatters them so that each queue's segment is longest-first.
+// `each(f, scatter)` must call f(item, cost, queue) once per item, the same
+// items with the same costs and queues in both passes (scatter = false:
+// counting, then true: placing).
 template <typename Item, typename Each>
 __device__ void build_queues(Each &&each, int32_t *hist, int32_t *part, int32_t *hdr, int base,
                              Item *out, int64_t max_items) {
@@ -68,7 +71,7 @@ __device__ void build_queues(Each &&each, int32_t *hist, int32_t *part, int32_t 
   __syncthreads();
   each([&](const Item &, int64_t cost, int x) {
     atomicAdd(&hist[x * kQBuckets + cost_bucket(cost)], 1);
-  });
+  }, false);
   __syncthreads();
   constexpr int per = kXcds * kQBuckets / kPrepThreads;
   int32_t s = 0;
@@ -103,7 +106,7 @@ __device__ void build_queues(Each &&each, int32_t *hist, int32_t *part, int32_t 
   each([&](const Item &it, int64_t cost, int x) {
     const int32_t p = atomicAdd(&hist[x * kQBuckets + cost_bucket(cost)], 1);
     if (p < max_items) out[p] = it;
-  });
+  }, true);
 }
 
 // The XCD this workgroup runs on, read from the hardware (XCC_ID, bits 3:0).
@@ -128,6 +131,11 @@ __device__ __forceinline__ int take_item(int32_t *hdr, int base, int &q, int &le
 
 // One forward work item: up to 4 query heads of one KV group x up to
 // 32 * (4 / heads) consecutive rows of one sample fragment of one tile.
+// An item walks the 64-key blocks [kb0, kb1) of its rows' sample; a whole
+// item has kb0 = 0 and kb1 = the blocks its last row attends.  A forward item
+// split into key ranges (split K) has one item per range, each writing its
+// unnormalised partial result to partial slot `slot` (-1: a whole item,
+// which writes O and LSE itself).
 struct FwdItem {
   int32_t q_row0;   // Q/O row of the first row
   int32_t q_loc0;   // sample-local position of the first row
@@ -136,8 +144,31 @@ struct FwdItem {
   int32_t nh;       // heads (1..4)
   int32_t nrows;    // rows (1..128)
   int32_t g;        // KV head
-  int32_t pad;
+  int32_t kb0;      // first key block
+  int32_t kb1;      // end of the key blocks
+  int32_t slot;     // partial slot of a split part, or -1
+  int32_t pad0, pad1;
 };
+static_assert(sizeof(FwdItem) == 48, "item layout");
+
+// A split forward item: the whole item (kb0 = 0, slot = -1) and the partial
+// slots [base, base + parts) of its parts, in key order.
+struct FwdSplit {
+  FwdItem item;
+  int32_t base;
+  int32_t parts;
+  int32_t pad0, pad1;
+};
+
+// Partial slots of split forward items: per slot, the unnormalised O of the
+// item's 4 waves x 32 rows (fp32, D per row), then the running max (log2
+// units) and the row sum of P of each of the 128 rows.
+constexpr int kFwdPartRows = 4 * 32;
+constexpr int kFwdSplitMinBlocks = 32;   // a part walks at least 32 key blocks (2048 keys)
+constexpr int kFwdSplitSlots = 3072;     // partial slots of one forward call
+__host__ __device__ constexpr size_t fwd_part_floats(int d) {
+  return (size_t)kFwdPartRows * (size_t)(d + 2);
+}
 
 // One backward work item: 128 keys (block kb, anchored at the sample start)
 // of KV head g of sample j.
@@ -480,16 +511,21 @@ __device__ __forceinline__ bool tile_ok(const libra_tile_t &t, int64_t n_q, int6
 // ---------------------------------------------------------------------------
 // Host-side workspace layouts and launchers (defined in attn_fwd.hip / attn_bwd.hip).
 struct FwdLayout {
-  size_t hdr = 0, items = 0, total = 0;
+  size_t hdr = 0, items = 0, splits = 0, parts = 0, total = 0;
   int64_t max_items = 0;
+  int32_t max_parts = 0;   // 0: items are never split
 };
 struct BwdLayout {
   size_t hdr = 0, ext = 0, gmask = 0, items = 0, qitems = 0, q16 = 0, do16 = 0, k16 = 0,
-         v16 = 0, stats = 0, aug = 0, total = 0;
+         v16 = 0, stats = 0, aug = 0, splits = 0, parts = 0, total = 0;
+  int32_t max_parts = 0;   // split-K partial slots of the dQ kernel
   int64_t max_items = 0, max_qitems = 0, nq_pad = 0;
 };
 
-FwdLayout fwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, int h_kv, int d);
+// `split`: room for split-K partial results (libra_attn_fwd); without it the
+// forward never splits an item (the allocation-free entry point).
+FwdLayout fwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, int h_kv, int d,
+                     bool split = true);
 BwdLayout bwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, int h_kv, int d);
 
 // Optional HIP events recorded around a main kernel (see libra_timing_*).
@@ -499,9 +535,15 @@ struct KernelTimer {
 
 // Shared preparation pass (attn_fwd.hip): forward-style work items, also
 // used by the dQ kernel.
+// Forward-style items for the dQ kernel's `grid` workgroups, split K as in
+// the forward when max_parts > 0 (split records into `splits`), but only when
+// whole rounds of items would leave workgroups idle: measured on calls of one
+// tile, splitting items that already fill the grid cost dQ 2-4%, while the
+// forward gained 3-5% from it.
 void enqueue_fwd_items(const int64_t *cu, int64_t n, const libra_tile_t *tiles, int64_t T,
                        int h_q, int h_kv, int64_t n_q, int64_t n_kv, int32_t *hdr,
-                       FwdItem *items, int64_t max_items, bool count_bad, hipStream_t st);
+                       FwdItem *items, int64_t max_items, bool count_bad, int grid,
+                       int max_parts, FwdSplit *splits, hipStream_t st);
 int64_t fwd_max_items(int64_t T, int64_t n, int64_t n_q, int h_q, int h_kv);
 
 int launch_fwd(const void *q, const void *k, const void *v, const int64_t *cu, int64_t n,
@@ -513,7 +555,8 @@ int launch_fwd(const void *q, const void *k, const void *v, const int64_t *cu, i
 int launch_bwd_dq(int d, const bf16 *q, const bf16 *dout, const bf16 *k, const bf16 *v,
                   const float *stats, const int64_t *cu, const FwdItem *items, int32_t *hdr,
                   int h_q, int h_kv, int64_t n_q, int64_t n_kv, int64_t nq_pad, float scale,
-                  bf16 *dq, f16 *aug, int blocks, hipStream_t st, const KernelTimer *tm);
+                  bf16 *dq, f16 *aug, const FwdSplit *splits, float *parts, int max_parts,
+                  int blocks, hipStream_t st, const KernelTimer *tm);
 int launch_bwd(const void *q, const void *k, const void *v, const void *o, const float *lse,
                const void *dout, const int64_t *cu, int64_t n, const libra_tile_t *tiles,
                int64_t T, int64_t n_q, int64_t n_kv, int h_q, int h_kv, int d, float scale,

@@ -54,8 +54,9 @@ __device__ void for_each_fwd_item_in(const libra_tile_t &t, int64_t wa, int64_t 
         for (; pb + k * rows_per < lim; ++k) {
           const int32_t rb = (int32_t)(k * rows_per);
           const int nrows = min(rows_per, nfrag - rb);
-          FwdItem it{row0 + rb, qloc0 + rb, (int32_t)j, h0, nh, nrows, g, 0};
-          f(it, (qloc0 + rb + nrows - 1) / kFwdBN + 1);
+          const int32_t nkb = (qloc0 + rb + nrows - 1) / kFwdBN + 1;
+          FwdItem it{row0 + rb, qloc0 + rb, (int32_t)j, h0, nh, nrows, g, 0, nkb, -1, 0, 0};
+          f(it, nkb);
         }
       }
     }
@@ -66,13 +67,28 @@ __device__ void for_each_fwd_item_in(const libra_tile_t &t, int64_t wa, int64_t 
 // by (KV head, head chunk) so that an XCD streams few K/V sequences.  Tiles
 // outside the buffers are skipped, and counted in hdr[kBadTiles] when
 // `count_bad` is set (the backward counts them in its own preparation pass).
+//
+// Split K: when there are fewer than two items per workgroup of the `grid`
+// that runs them (few rows and heads against long samples), and with
+// `idle_only` only when whole rounds of `grid` items would leave more than a
+// tenth of the workgroups idle, the key blocks that all rows of an item
+// attend in full (below its first row's block kd) are cut into ranges of C
+// blocks, about four items per workgroup in all;
+// the last range also takes the blocks from kd on, so that every row has a
+// key in the first block of every range.  Items with kd < 2 C stay whole.
+// Each part writes a partial result to its own slot (max_parts slots;
+// max_parts = 0 never splits) and fwd_combine_kernel merges the parts of
+// every split item.  C is at least kFwdSplitMinBlocks and doubles until the
+// parts fit the slots.
 __global__ __launch_bounds__(kPrepThreads) void prep_fwd_kernel(
     const int64_t *__restrict__ cu, int64_t n, const libra_tile_t *__restrict__ tiles, int64_t T,
     int h_q, int h_kv, int64_t n_q, int64_t n_kv, int32_t *__restrict__ hdr,
-    FwdItem *__restrict__ items, int64_t max_items, int count_bad) {
+    FwdItem *__restrict__ items, int64_t max_items, int count_bad, int grid, int max_parts,
+    int idle_only, FwdSplit *__restrict__ splits) {
   __shared__ int32_t hist[kXcds * kQBuckets];
   __shared__ int32_t part[kPrepThreads];
-  __shared__ unsigned long long s_wmax;
+  __shared__ unsigned long long s_wmax, s_items, s_work, s_parts;
+  __shared__ int32_t s_chunk, s_nslot, s_nsplit;
   const int tid = threadIdx.x;
   const int G = h_q / h_kv;
   const int chunks = (G + 3) / 4;                    // head chunks per KV group
@@ -80,7 +96,14 @@ __global__ __launch_bounds__(kPrepThreads) void prep_fwd_kernel(
   const int R = keys >= kXcds ? 1 : kXcds / keys;    // queues per key
   if (tid == 0) {
     if (count_bad) hdr[kBadTiles] = 0;
+    hdr[kFwdSplits] = 0;
+    hdr[kFwdSplits + 1] = 0;
     s_wmax = 0;
+    s_items = 0;
+    s_work = 0;
+    s_chunk = 0;
+    s_nslot = 0;
+    s_nsplit = 0;
   }
   __threadfence();
   __syncthreads();
@@ -100,7 +123,8 @@ __global__ __launch_bounds__(kPrepThreads) void prep_fwd_kernel(
   if (wm) atomicMax(&s_wmax, wm);
   __syncthreads();
   const int64_t wmax = (int64_t)s_wmax;
-  auto each = [&](auto &&f) {
+  // every whole item once: f(item, queue)
+  auto whole = [&](auto &&f) {
     for (int64_t v = tid; v < T * wmax; v += kPrepThreads) {
       const int64_t t = v / wmax, w = v % wmax;
       const libra_tile_t tl = tiles[t];
@@ -108,14 +132,126 @@ __global__ __launch_bounds__(kPrepThreads) void prep_fwd_kernel(
       const int64_t wa = tl.q_begin + (int64_t)kRows * w;
       if (wa >= tl.q_end) continue;
       const int64_t wb = wa + kRows < tl.q_end ? wa + kRows : tl.q_end;
-      for_each_fwd_item_in(tl, wa, wb, cu, n, G, [&](const FwdItem &it, int nkb) {
+      for_each_fwd_item_in(tl, wa, wb, cu, n, G, [&](const FwdItem &it, int) {
         const int key = it.g * chunks + (it.head0 - it.g * G) / 4;
-        const int x = (key * R + (it.q_row0 / 128) % R) % kXcds;
-        f(it, (int64_t)nkb, x);
+        f(it, (key * R + (it.q_row0 / 128) % R) % kXcds);
       });
     }
   };
+  if (max_parts > 0) {
+    whole([&](const FwdItem &it, int) {
+      atomicAdd(&s_items, 1ull);
+      atomicAdd(&s_work, (unsigned long long)it.kb1);
+    });
+    __syncthreads();
+    const unsigned long long n_items = s_items, work = s_work, gr = (unsigned long long)grid;
+    // rounds of `grid` items fill less than 90% of the workgroups
+    const bool idle = n_items * 10 < (n_items + gr - 1) / gr * gr * 9;
+    if (n_items > 0 && n_items < 2 * gr && (idle || !idle_only)) {
+      long long c = (long long)((work + 4ull * grid - 1) / (4ull * grid));
+      c = c > kFwdSplitMinBlocks ? c : kFwdSplitMinBlocks;
+      for (; c < (1ll << 30); c *= 2) {   // at most ~30 rounds; the first fits by construction
+        if (tid == 0) s_parts = 0;
+        __syncthreads();
+        whole([&](const FwdItem &it, int) {
+          const long long np = (it.q_loc0 / kFwdBN) / c;
+          if (np >= 2) atomicAdd(&s_parts, (unsigned long long)np);
+        });
+        __syncthreads();
+        const bool fits = s_parts <= (unsigned long long)max_parts;
+        __syncthreads();
+        if (fits) break;
+      }
+      if (tid == 0) s_chunk = (int32_t)(c < (1ll << 30) ? c : 0);
+    }
+    __syncthreads();
+  }
+  const int chunk = s_chunk;   // 0: no item is split
+  auto each = [&](auto &&f, bool scatter) {
+    whole([&](const FwdItem &it, int x) {
+      const int np = chunk ? (it.q_loc0 / kFwdBN) / chunk : 0;
+      if (np < 2) {
+        f(it, (int64_t)it.kb1, x);
+        return;
+      }
+      int32_t base = 0;
+      if (scatter) {
+        base = atomicAdd(&s_nslot, np);
+        splits[atomicAdd(&s_nsplit, 1)] = FwdSplit{it, base, np, 0, 0};
+      }
+      for (int p = 0; p < np; ++p) {
+        FwdItem ip = it;
+        ip.kb0 = p * chunk;
+        ip.kb1 = p + 1 < np ? (p + 1) * chunk : it.kb1;
+        ip.slot = base + p;
+        f(ip, (int64_t)(ip.kb1 - ip.kb0), x);
+      }
+    });
+  };
   build_queues<FwdItem>(each, hist, part, hdr, kFwdQ, items, max_items);
+  __syncthreads();
+  if (tid == 0) {
+    hdr[kFwdSplits] = s_nsplit;
+    hdr[kFwdSplits + 1] = s_nslot;
+  }
+}
+
+// Merges the parts of every split item (hdr[kFwdSplits] records): per row,
+// m = max_p m_p, l = sum_p l_p 2^(m_p - m), O = sum_p O_p 2^(m_p - m) / l and
+// LSE = (m + log2 l) ln 2, the online-softmax recurrence applied across the
+// key ranges.  Two threads per row (half of the head dimension each).
+template <int D>
+__global__ __launch_bounds__(256) void fwd_combine_kernel(
+    const FwdSplit *__restrict__ splits, const int32_t *__restrict__ hdr,
+    const float *__restrict__ parts, int h_q, int64_t n_q, bf16 *__restrict__ o,
+    float *__restrict__ lse) {
+  constexpr size_t PF = fwd_part_floats(D);
+  const int count = hdr[kFwdSplits];
+  const int tid = threadIdx.x, pr = tid >> 1, half = tid & 1;
+  const int w = pr >> 5, r = pr & 31;   // wave slice and row of the item
+  for (int e = blockIdx.x; e < count; e += gridDim.x) {
+    const FwdSplit sp = splits[e];
+    const FwdItem &it = sp.item;
+    const int wrow0 = (w / it.nh) * kRows;
+    const int wrows = min(max(it.nrows - wrow0, 0), kRows);
+    if (r >= wrows) continue;
+    const int head = it.head0 + (w % it.nh);
+    const int64_t row = (int64_t)it.q_row0 + wrow0 + r;
+    float m = -INFINITY;
+    for (int p = 0; p < sp.parts; ++p) {
+      const float *rec = parts + (size_t)(sp.base + p) * PF + (size_t)kFwdPartRows * D;
+      m = fmaxf(m, rec[pr]);
+    }
+    float l = 0.f;
+    float acc[D / 2];
+#pragma unroll
+    for (int i = 0; i < D / 2; ++i) acc[i] = 0.f;
+    for (int p = 0; p < sp.parts; ++p) {
+      const float *rec = parts + (size_t)(sp.base + p) * PF;
+      const float mp = rec[(size_t)kFwdPartRows * D + pr];
+      const float wgt = mp == -INFINITY ? 0.f : fast_exp2(mp - m);
+      l += wgt * rec[(size_t)kFwdPartRows * D + kFwdPartRows + pr];
+      const float4 *src = reinterpret_cast<const float4 *>(rec + (size_t)pr * D + half * (D / 2));
+#pragma unroll
+      for (int i = 0; i < D / 8; ++i) {
+        const float4 x = src[i];
+        acc[4 * i] += wgt * x.x;
+        acc[4 * i + 1] += wgt * x.y;
+        acc[4 * i + 2] += wgt * x.z;
+        acc[4 * i + 3] += wgt * x.w;
+      }
+    }
+    const float inv = 1.f / l;
+    bf16 *op = o + ((size_t)row * h_q + head) * D + half * (D / 2);
+#pragma unroll
+    for (int i = 0; i < D / 16; ++i) {
+      bf16x8 ov;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) ov[j] = static_cast<bf16>(acc[8 * i + j] * inv);
+      *reinterpret_cast<bf16x8 *>(op + 8 * i) = ov;
+    }
+    if (half == 0) lse[(size_t)head * n_q + row] = (m + __builtin_amdgcn_logf(l)) * kLn2;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -133,7 +269,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     const bf16 *__restrict__ q, const bf16 *__restrict__ k, const bf16 *__restrict__ v,
     const int64_t *__restrict__ cu, const FwdItem *__restrict__ items, int32_t *__restrict__ hdr,
     int h_q, int h_kv, int64_t n_q, int64_t n_kv, float c2,
-    bf16 *__restrict__ o, float *__restrict__ lse) {
+    bf16 *__restrict__ o, float *__restrict__ lse, float *__restrict__ parts) {
   using S = FwdShape<D>;
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
   __shared__ int32_t s_item;
@@ -179,7 +315,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     const int64_t row = (int64_t)it.q_row0 + wrow0 + my_r;
     const int qloc = it.q_loc0 + wrow0 + my_r;
     const int wave_qmin = it.q_loc0 + wrow0;
-    const int nkb = (it.q_loc0 + it.nrows - 1) / kFwdBN + 1;
+    const int kb0 = it.kb0, nkb = it.kb1;   // key blocks [kb0, nkb)
     const int wave_nkb = active ? (it.q_loc0 + wrow0 + wrows - 1) / kFwdBN + 1 : 0;
 
     bf16x8 qf[D / 16];
@@ -197,11 +333,11 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     auto issue = [&](int b, int buf, int part) {
       const bf16 *src = part ? v : k;
       bf16 *dst = smem + buf * S::STAGE + part * S::K_EL;
-      const int64_t kb0 = key0 + (int64_t)b * kFwdBN;
-      if (kb0 + kFwdBN <= n_kv) {
+      const int64_t kbase = key0 + (int64_t)b * kFwdBN;
+      if (kbase + kFwdBN <= n_kv) {
         // whole block inside the buffer: one SGPR base, fixed per-lane offsets;
         // wave load u lands 1 KiB x (w + kWaves u) into the tile
-        const bf16 *base = src + ((size_t)kb0 * h_kv + it.g) * D;
+        const bf16 *base = src + ((size_t)kbase * h_kv + it.g) * D;
         const uint32_t ld = lds_addr(dst) + 1024u * w;
         static_for<S::NK / 4>([&](auto h) {
           constexpr uint32_t d = 4 * h * kWaves * 1024u, e = kWaves * 1024u;
@@ -225,12 +361,12 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
       });
     };
 
-    issue(0, 0, 0);
-    issue(0, 0, 1);
+    issue(kb0, 0, 0);
+    issue(kb0, 0, 1);
     wait_vm();
     __syncthreads();
-    for (int b = 0; b < nkb; ++b) {
-      const int buf = b & 1;
+    for (int b = kb0; b < nkb; ++b) {
+      const int buf = (b - kb0) & 1;
       // the next block's K rows now, its V rows after this block's S^T
       // products (the other workgroup on the CU keeps the matrix cores busy
       // while this one waits to issue)
@@ -277,7 +413,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
           });
         };
         bool move = true;
-        if (b > 0) {
+        if (b > kb0) {
           expo(-m_run);
           move = !(row_sum2(ps) <= 256.f);
         }
@@ -309,7 +445,30 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
       __syncthreads();
     }
 
-    if (active) {
+    if (active && it.slot >= 0) {
+      // a part of a split item: unnormalised O, the running max and the row
+      // sum into its partial slot (rows w * 32 + ln), merged by
+      // fwd_combine_kernel
+      const float l_tot = row_sum2(l_run);
+      if (ln < wrows) {
+        float *rec = parts + (size_t)it.slot * fwd_part_floats(D);
+        float *op = rec + (size_t)(w * kRows + ln) * D + 8 * kg;
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            float4 *dst = reinterpret_cast<float4 *>(op + 32 * dt + 16 * hh);
+            dst[0] = make_float4(oacc[dt][8 * hh], oacc[dt][8 * hh + 1], oacc[dt][8 * hh + 2],
+                                 oacc[dt][8 * hh + 3]);
+            dst[1] = make_float4(oacc[dt][8 * hh + 4], oacc[dt][8 * hh + 5],
+                                 oacc[dt][8 * hh + 6], oacc[dt][8 * hh + 7]);
+          }
+        if (kg == 0) {
+          rec[(size_t)kFwdPartRows * D + w * kRows + ln] = m_run;
+          rec[(size_t)kFwdPartRows * D + kFwdPartRows + w * kRows + ln] = l_tot;
+        }
+      }
+    } else if (active) {
       const float l_tot = row_sum2(l_run);
       const float inv = 1.f / l_tot;
       if (ln < wrows) {
@@ -336,16 +495,22 @@ static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 int64_t fwd_max_items(int64_t T, int64_t n, int64_t n_q, int h_q, int h_kv) {
   // items <= rows*heads/64 (an item covers >= 64 (row, head) pairs or ends a
   // fragment) + fragments * head chunks.
+  // A split item's parts take its place: kFwdSplitSlots of them at most.
   const int64_t frags = T + (int64_t)h_q * n;
-  return n_q * (int64_t)h_q / 64 + frags * (int64_t)(h_kv + h_q / 4 + 1) + 1;
+  return n_q * (int64_t)h_q / 64 + frags * (int64_t)(h_kv + h_q / 4 + 1) + 1 + kFwdSplitSlots;
 }
 
-FwdLayout fwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, int h_kv, int d) {
+FwdLayout fwd_layout(int64_t T, int64_t n, int64_t n_q, int64_t n_kv, int h_q, int h_kv, int d,
+                     bool split) {
   FwdLayout L;
   L.max_items = fwd_max_items(T, n, n_q, h_q, h_kv);
   L.hdr = 0;
   L.items = align256(kHdrSlots * sizeof(int32_t));
-  L.total = align256(L.items + (size_t)L.max_items * sizeof(FwdItem));
+  L.splits = align256(L.items + (size_t)L.max_items * sizeof(FwdItem));
+  L.max_parts = split ? kFwdSplitSlots : 0;
+  // a split item has at least two parts
+  L.parts = align256(L.splits + (size_t)(L.max_parts / 2) * sizeof(FwdSplit));
+  L.total = align256(L.parts + (size_t)L.max_parts * fwd_part_floats(d) * sizeof(float));
   return L;
 }
 
@@ -356,6 +521,8 @@ static int launch_fwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const int64
                         char *ws, const FwdLayout &L, hipStream_t st, const KernelTimer *tm) {
   int32_t *hdr = reinterpret_cast<int32_t *>(ws + L.hdr);
   FwdItem *items = reinterpret_cast<FwdItem *>(ws + L.items);
+  auto *splits = reinterpret_cast<FwdSplit *>(ws + L.splits);
+  float *parts = reinterpret_cast<float *>(ws + L.parts);
   static bool attr_set = false;
   if (!attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void *>(&attn_fwd_kernel<D>),
@@ -364,15 +531,19 @@ static int launch_fwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const int64
       return fail(LIBRA_EHIP, "hipFuncSetAttribute failed");
     attr_set = true;
   }
-  hipLaunchKernelGGL(prep_fwd_kernel, dim3(1), dim3(kPrepThreads), 0, st, cu, n, tiles, T, h_q,
-                     h_kv, n_q, n_kv, hdr, items, L.max_items, 1);
   int dev = 0, cus = 256;
   hipGetDevice(&dev);
   hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  const int grid = cus * 2;
+  hipLaunchKernelGGL(prep_fwd_kernel, dim3(1), dim3(kPrepThreads), 0, st, cu, n, tiles, T, h_q,
+                     h_kv, n_q, n_kv, hdr, items, L.max_items, 1, grid, L.max_parts, 0, splits);
   if (tm) hipEventRecord(tm->begin, st);
-  hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3(cus * 2), dim3(kThreads), FwdShape<D>::SMEM, st, q,
+  hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3(grid), dim3(kThreads), FwdShape<D>::SMEM, st, q,
                      k, v, cu, items, hdr, h_q, h_kv, n_q, n_kv, scale * kLog2e, o,
-                     lse);
+                     lse, parts);
+  if (L.max_parts > 0)
+    hipLaunchKernelGGL(fwd_combine_kernel<D>, dim3(cus), dim3(256), 0, st, splits, hdr, parts,
+                       h_q, n_q, o, lse);
   if (tm) hipEventRecord(tm->end, st);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(LIBRA_EHIP, "forward launch failed: %s", hipGetErrorString(e));
@@ -381,9 +552,11 @@ static int launch_fwd_d(const bf16 *q, const bf16 *k, const bf16 *v, const int64
 
 void enqueue_fwd_items(const int64_t *cu, int64_t n, const libra_tile_t *tiles, int64_t T,
                        int h_q, int h_kv, int64_t n_q, int64_t n_kv, int32_t *hdr,
-                       FwdItem *items, int64_t max_items, bool count_bad, hipStream_t st) {
+                       FwdItem *items, int64_t max_items, bool count_bad, int grid,
+                       int max_parts, FwdSplit *splits, hipStream_t st) {
   hipLaunchKernelGGL(prep_fwd_kernel, dim3(1), dim3(kPrepThreads), 0, st, cu, n, tiles, T, h_q,
-                     h_kv, n_q, n_kv, hdr, items, max_items, count_bad ? 1 : 0);
+                     h_kv, n_q, n_kv, hdr, items, max_items, count_bad ? 1 : 0, grid, max_parts,
+                     1, splits);
 }
 
 int launch_fwd(const void *q, const void *k, const void *v, const int64_t *cu, int64_t n,

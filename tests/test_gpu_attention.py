@@ -43,6 +43,76 @@ def test_fwd_small_random(seed):
     check("LSE", to_np(lse), LSE, (LSE_TOL, 1e-4))
 
 
+def _span_tiles(spans):
+    """Hand-made tiles over one sample: (q_begin, q_end, head_begin, head_end)
+    each, Q rows in span order.  Returns the tiles and the rows' positions."""
+    tiles = np.zeros(len(spans), dtype=pl.TILE_DTYPE)
+    pos, row = [], 0
+    for i, (b, e, hb, he) in enumerate(spans):
+        tiles[i] = (b, e, row, 0, hb, he, 0, 0, 0, i)
+        pos.extend(range(b, e))
+        row += e - b
+    return tiles, np.asarray(pos, dtype=np.int64)
+
+
+@pytest.mark.parametrize("h_q,h_kv,d", [(4, 2, 128), (8, 1, 64)])
+def test_fwd_split_k_few_rows_long_sample(h_q, h_kv, d):
+    """Few rows and heads against a 65,536-token sample: fewer work items than
+    workgroups, so the forward cuts them into key ranges (split K) and merges
+    the partial results.  O and LSE of the covered pairs against the oracle."""
+    L = 65536
+    spans = [(L - 256, L, 0, 2), (30000, 30128, 2, 4), (4100, 4200, 0, 1)]
+    tiles, pos = _span_tiles(spans)
+    n_q = len(pos)
+    say(f"[fwd split K] sample {L} rows={n_q} heads=({h_q},{h_kv}) d={d}")
+    q, k, v, _ = wl.tensors(7, n_q, L, h_q, h_kv, d, with_dout=False)
+    cu = torch.tensor([0, L], dtype=torch.int64, device=DEV)
+    o = torch.zeros((n_q, h_q, d), dtype=torch.bfloat16, device=DEV)
+    lse = torch.zeros((h_q, n_q), dtype=torch.float32, device=DEV)
+    qd, kd, vd = _dev(q, k, v)
+    pl.libra_attn_fwd(qd, kd, vd, cu, pl.tiles_to_device(tiles, DEV), o=o, lse=lse)
+    torch.cuda.synchronize()
+    O, LSE = oa.attention_fwd(q, k, v, [L], pos, heads=range(4))
+    cov = _coverage(tiles, n_q, h_q)
+    check("O", to_np(o)[cov], O[cov], bf16_out=True)
+    check("LSE", to_np(lse).T[cov], LSE.T[cov], (LSE_TOL, 1e-4))
+
+
+@pytest.mark.parametrize("h_q,h_kv,d", [(4, 2, 128), (8, 1, 64)])
+def test_bwd_split_k_few_rows_long_sample(h_q, h_kv, d):
+    """The split-K case of the forward test above through the backward: the
+    dQ kernel's items split the same way, and its merge writes dQ and the
+    -D records that the dK / dV kernel reads.  dQ of the covered pairs and
+    dK / dV (bf16 and fp32) against the oracle, with dO zero outside them."""
+    L = 65536
+    spans = [(L - 256, L, 0, 2), (30000, 30128, 2, 4), (4100, 4200, 0, 1)]
+    tiles, pos = _span_tiles(spans)
+    n_q = len(pos)
+    say(f"[bwd split K] sample {L} rows={n_q} heads=({h_q},{h_kv}) d={d}")
+    q, k, v, do = wl.tensors(8, n_q, L, h_q, h_kv, d)
+    cov = torch.from_numpy(_coverage(tiles, n_q, h_q))[:, :, None]
+    do = torch.where(cov, do, torch.zeros_like(do))
+    cu = torch.tensor([0, L], dtype=torch.int64, device=DEV)
+    qd, kd, vd, dod = _dev(q, k, v, do)
+    td = pl.tiles_to_device(tiles, DEV)
+    o = torch.zeros((n_q, h_q, d), dtype=torch.bfloat16, device=DEV)
+    lse = torch.zeros((h_q, n_q), dtype=torch.float32, device=DEV)
+    pl.libra_attn_fwd(qd, kd, vd, cu, td, o=o, lse=lse)
+    dq = torch.zeros_like(qd)
+    dq, dk, dv = pl.libra_attn_bwd(qd, kd, vd, o, lse, dod, cu, td, dq=dq)
+    dk32 = torch.zeros(kd.shape, dtype=torch.float32, device=DEV)
+    dv32 = torch.zeros_like(dk32)
+    pl.libra_attn_bwd(qd, kd, vd, o, lse, dod, cu, td, dk=dk32, dv=dv32, accumulate=True)
+    torch.cuda.synchronize()
+    dQ, dK, dV = oa.attention_bwd(q, k, v, do, [L], pos)
+    c = cov.expand_as(q).numpy()
+    check("dQ covered", to_np(dq)[c], np.asarray(dQ)[c], bf16_out=True)
+    check("dK", to_np(dk), dK, bf16_out=True)
+    check("dV", to_np(dv), dV, bf16_out=True)
+    check("dK fp32", to_np(dk32), dK)
+    check("dV fp32", to_np(dv32), dV)
+
+
 @pytest.mark.parametrize("seed", range(16))
 def test_bwd_small_random(seed):
     w = wl.small_random(seed)
@@ -229,6 +299,54 @@ def test_bwd_per_worker_accumulate(seed):
     check("dQ", to_np(dq), dQ, bf16_out=True)
     check("dK", to_np(dk), dK)
     check("dV", to_np(dv), dV)
+
+
+def _coverage(tiles, n_q, h_q):
+    """(row, head) pairs that a tile list covers."""
+    m = np.zeros((n_q, h_q), dtype=bool)
+    for t in tiles:
+        r0 = int(t["q_row"])
+        m[r0:r0 + int(t["q_end"]) - int(t["q_begin"]), int(t["head_begin"]):int(t["head_end"])] = True
+    return m
+
+
+@pytest.mark.parametrize("seed", [200, 203, 207, 210, 211])
+def test_bwd_ignores_uncovered_rows(seed):
+    """One virtual worker's tile set, with NaN in every (row, head) of Q and
+    dO that its tiles do not cover: dK / dV (bf16 and fp32) and the covered
+    dQ match the oracle run with dO = 0 outside the covered pairs.  The
+    dK / dV kernel stages whole 32-row blocks, so this checks that rows
+    outside the tiles never reach its products."""
+    w = wl.small_random(seed)
+    w.CP = 2 if all(p % 4 == 0 for p in w.pack_tokens) else 1
+    tiles, _ = plan(w)
+    counts = np.bincount(tiles["worker"], minlength=w.V)
+    mine = tiles[tiles["worker"] == int(np.argmax(counts))]
+    say(f"[bwd uncovered NaN {seed}] packs={w.pack_tokens} V={w.V} tiles={len(mine)} "
+        f"heads=({w.h_q},{w.h_kv}) d={w.d}")
+    q, k, v, do = _inputs(w)
+    cov = torch.from_numpy(_coverage(mine, w.n_q_rows, w.h_q))[:, :, None]
+    nan = torch.tensor(float("nan"), dtype=q.dtype)
+    qd, kd, vd, dod = _dev(torch.where(cov, q, nan), k, v, torch.where(cov, do, nan))
+    cu = cu_dev(w)
+    td = pl.tiles_to_device(mine, DEV)
+    o = torch.zeros_like(qd)
+    lse = torch.zeros((w.h_q, w.n_q_rows), device=DEV)
+    pl.libra_attn_fwd(qd, kd, vd, cu, td, o=o, lse=lse)
+    dq = torch.zeros_like(qd)
+    dq, dk, dv = pl.libra_attn_bwd(qd, kd, vd, o, lse, dod, cu, td, dq=dq)
+    dk32 = torch.zeros(kd.shape, dtype=torch.float32, device=DEV)
+    dv32 = torch.zeros_like(dk32)
+    pl.libra_attn_bwd(qd, kd, vd, o, lse, dod, cu, td, dk=dk32, dv=dv32, accumulate=True)
+    torch.cuda.synchronize()
+    dQ, dK, dV = oa.attention_bwd(q, k, v, torch.where(cov, do, torch.zeros_like(do)),
+                                  w.lengths, w.q_positions())
+    c = cov.expand_as(q).numpy()
+    check("dQ covered", to_np(dq)[c], np.asarray(dQ)[c], bf16_out=True)
+    check("dK", to_np(dk), dK, bf16_out=True)
+    check("dV", to_np(dv), dV, bf16_out=True)
+    check("dK fp32", to_np(dk32), dK)
+    check("dV fp32", to_np(dv32), dV)
 
 
 def test_empty_tile_list():
