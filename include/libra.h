@@ -170,9 +170,16 @@ size_t libra_attn_workspace_size(int64_t num_tiles, int64_t num_samples, int64_t
  *   o [n_q_rows][h_q][d] bf16, lse [h_q][n_q_rows] fp32: device outputs; only
  *       covered (row, head) entries are written.
  *   workspace: device, >= libra_attn_workspace_size(..., 0) bytes, 256-byte
- *       aligned; contents are scratch.
+ *       aligned; contents are scratch.  It holds the work items and the
+ *       split-K partial results (3072 slots of 128 rows x (d + 2) fp32, about
+ *       200 MB at d = 128).
+ * Split K: a call with fewer than two work items per workgroup (few rows and
+ * heads against long samples) cuts its long items into key ranges that run in
+ * parallel and merges their partial results (the online-softmax recurrence
+ * across ranges); the result is the same up to the order of fp32 additions.
  * Rows and heads are processed independently of how tiles group them, so the
- * output does not depend on B, H or the worker a tile was placed on.
+ * output does not depend on B, H or the worker a tile was placed on; it is
+ * bit-identical across such groupings whenever no item is split.
  */
 int libra_attn_fwd(const void *q, const void *k, const void *v, const int64_t *cu_seqlens,
                    int64_t num_samples, const libra_tile_t *tiles, int64_t num_tiles,
@@ -207,14 +214,17 @@ int libra_attn_skipped_tiles(const void *workspace, int32_t *count, void *stream
  * libra_attn_fwd_noalloc -- libra_attn_fwd without a workspace argument, for
  * callers that cannot allocate device memory (code under HIP graph capture,
  * tight serving loops, harnesses that forbid allocation).  Same arguments,
- * semantics and errors as libra_attn_fwd, with the same kernels; the work
- * items live in a device array built into the library, of
- * LIBRA_FWD_NOALLOC_MAX_WORKSPACE bytes, one per device, held until the
- * process ends.  The call allocates nothing and frees nothing (its first
- * call on a device looks up that device's array).
- *   Sizes whose libra_attn_workspace_size(..., 0) exceeds the array are
- *   rejected with LIBRA_ENOSPC before anything is enqueued (16 MiB covers,
- *   e.g., 65536 query rows x 32 heads of a 1M-token pack).
+ * semantics and errors as libra_attn_fwd, with the same kernels but without
+ * split K (its partial slots would not fit), so its results equal
+ * libra_attn_fwd's whenever that call splits no item; the work items live in
+ * a device array built into the library, of LIBRA_FWD_NOALLOC_MAX_WORKSPACE
+ * bytes, one per device, held until the process ends.  The call allocates
+ * nothing and frees nothing (its first call on a device looks up that
+ * device's array).
+ *   Sizes whose work-item list (48 bytes per item, bounded from the sizes as
+ *   for libra_attn_workspace_size) exceeds the array are rejected with
+ *   LIBRA_ENOSPC before anything is enqueued (16 MiB covers, e.g., 65536
+ *   query rows x 32 heads of a 1M-token pack).
  *   Every call on one device shares that device's array: calls that overlap
  *   in time on one device (different streams, or host threads) race and
  *   must be serialized by the caller.  Each call's preparation pass rewrites
@@ -254,6 +264,10 @@ int libra_attn_fwd_noalloc(const void *q, const void *k, const void *v,
  * q, dout, o and lse in the covered (row, head) pairs, must be finite.
  * Other rows of q, dout, o and lse are not read by the dK / dV products
  * (their fp16 copies hold zeros there).
+ * Split K: the dQ products split their work items into key ranges as the
+ * forward does, when the call's items would leave more than a tenth of the
+ * workgroups idle; the parts' fp32 dQ and sums of dS are merged before the
+ * dK / dV products read D.  The workspace holds those partial results too.
  */
 int libra_attn_bwd(const void *q, const void *k, const void *v, const void *o, const float *lse,
                    const void *dout, const int64_t *cu_seqlens, int64_t num_samples,
