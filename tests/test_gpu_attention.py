@@ -70,8 +70,14 @@ def test_fwd_split_k_few_rows_long_sample(h_q, h_kv, d):
     o = torch.zeros((n_q, h_q, d), dtype=torch.bfloat16, device=DEV)
     lse = torch.zeros((h_q, n_q), dtype=torch.float32, device=DEV)
     qd, kd, vd = _dev(q, k, v)
-    pl.libra_attn_fwd(qd, kd, vd, cu, pl.tiles_to_device(tiles, DEV), o=o, lse=lse)
+    td = pl.tiles_to_device(tiles, DEV)
+    pl.libra_attn_fwd(qd, kd, vd, cu, td, o=o, lse=lse)
+    o2, lse2 = torch.zeros_like(o), torch.zeros_like(lse)
+    pl.libra_attn_fwd(qd, kd, vd, cu, td, o=o2, lse=lse2)
     torch.cuda.synchronize()
+    # the parts are merged in key order: the result does not depend on which
+    # workgroup ran which part
+    assert torch.equal(o, o2) and torch.equal(lse, lse2), "split-K forward not deterministic"
     O, LSE = oa.attention_fwd(q, k, v, [L], pos, heads=range(4))
     cov = _coverage(tiles, n_q, h_q)
     check("O", to_np(o)[cov], O[cov], bf16_out=True)
@@ -100,10 +106,14 @@ def test_bwd_split_k_few_rows_long_sample(h_q, h_kv, d):
     pl.libra_attn_fwd(qd, kd, vd, cu, td, o=o, lse=lse)
     dq = torch.zeros_like(qd)
     dq, dk, dv = pl.libra_attn_bwd(qd, kd, vd, o, lse, dod, cu, td, dq=dq)
+    dq2 = torch.zeros_like(qd)
+    dq2, dk2, dv2 = pl.libra_attn_bwd(qd, kd, vd, o, lse, dod, cu, td, dq=dq2)
     dk32 = torch.zeros(kd.shape, dtype=torch.float32, device=DEV)
     dv32 = torch.zeros_like(dk32)
     pl.libra_attn_bwd(qd, kd, vd, o, lse, dod, cu, td, dk=dk32, dv=dv32, accumulate=True)
     torch.cuda.synchronize()
+    assert torch.equal(dq, dq2) and torch.equal(dk, dk2) and torch.equal(dv, dv2), \
+        "split-K backward not deterministic"
     dQ, dK, dV = oa.attention_bwd(q, k, v, do, [L], pos)
     c = cov.expand_as(q).numpy()
     check("dQ covered", to_np(dq)[c], np.asarray(dQ)[c], bf16_out=True)
