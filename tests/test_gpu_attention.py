@@ -55,7 +55,7 @@ def _span_tiles(spans):
     return tiles, np.asarray(pos, dtype=np.int64)
 
 
-@pytest.mark.parametrize("h_q,h_kv,d", [(4, 2, 128), (8, 1, 64)])
+@pytest.mark.parametrize("h_q,h_kv,d", [(4, 2, 128), (8, 1, 64), (6, 2, 64)])
 def test_fwd_split_k_few_rows_long_sample(h_q, h_kv, d):
     """Few rows and heads against a 65,536-token sample: fewer work items than
     workgroups, so the forward cuts them into key ranges (split K) and merges
@@ -84,7 +84,7 @@ def test_fwd_split_k_few_rows_long_sample(h_q, h_kv, d):
     check("LSE", to_np(lse).T[cov], LSE.T[cov], (LSE_TOL, 1e-4))
 
 
-@pytest.mark.parametrize("h_q,h_kv,d", [(4, 2, 128), (8, 1, 64)])
+@pytest.mark.parametrize("h_q,h_kv,d", [(4, 2, 128), (8, 1, 64), (6, 2, 64)])
 def test_bwd_split_k_few_rows_long_sample(h_q, h_kv, d):
     """The split-K case of the forward test above through the backward: the
     dQ kernel's items split the same way, and its merge writes dQ and the
