@@ -87,7 +87,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_fwd_kernel(
     int idle_only, FwdSplit *__restrict__ splits) {
   __shared__ int32_t hist[kXcds * kQBuckets];
   __shared__ int32_t part[kPrepThreads];
-  __shared__ unsigned long long s_wmax, s_items, s_work, s_parts;
+  __shared__ unsigned long long s_wmax, s_items, s_work, s_parts, s_pairs;
   __shared__ int32_t s_chunk, s_nslot, s_nsplit;
   const int tid = threadIdx.x;
   const int G = h_q / h_kv;
@@ -99,6 +99,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_fwd_kernel(
     hdr[kFwdSplits] = 0;
     hdr[kFwdSplits + 1] = 0;
     s_wmax = 0;
+    s_pairs = 0;
     s_items = 0;
     s_work = 0;
     s_chunk = 0;
@@ -109,7 +110,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_fwd_kernel(
   __syncthreads();
   // bad tiles, and the 32-row windows of the longest good tile
   int bad = 0;
-  unsigned long long wm = 0;
+  unsigned long long wm = 0, pairs = 0;
   for (int64_t t = tid; t < T; t += kPrepThreads) {
     const libra_tile_t tl = tiles[t];
     if (!tile_ok(tl, n_q, n_kv, h_q)) {
@@ -118,9 +119,11 @@ __global__ __launch_bounds__(kPrepThreads) void prep_fwd_kernel(
     }
     const unsigned long long w = (unsigned long long)((tl.q_end - tl.q_begin + kRows - 1) / kRows);
     wm = w > wm ? w : wm;
+    pairs += (unsigned long long)(tl.q_end - tl.q_begin) * (unsigned long long)(tl.head_end - tl.head_begin);
   }
   if (bad && count_bad) atomicAdd(&hdr[kBadTiles], bad);
   if (wm) atomicMax(&s_wmax, wm);
+  if (pairs) atomicAdd(&s_pairs, pairs);
   __syncthreads();
   const int64_t wmax = (int64_t)s_wmax;
   // every whole item once: f(item, queue)
@@ -138,7 +141,9 @@ __global__ __launch_bounds__(kPrepThreads) void prep_fwd_kernel(
       });
     }
   };
-  if (max_parts > 0) {
+  // an item covers at most 128 (row, head) pairs: with pairs / 128 items or
+  // more there are enough for the grid, and the item count is not needed
+  if (max_parts > 0 && s_pairs / 128 < 2ull * (unsigned long long)grid) {
     whole([&](const FwdItem &it, int) {
       atomicAdd(&s_items, 1ull);
       atomicAdd(&s_work, (unsigned long long)it.kb1);
