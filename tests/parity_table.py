@@ -3,7 +3,10 @@ LIBRA_PARITY_LOG (one JSON object per check) as a Markdown table: per test
 and output, the max-abs error, the part of it beyond bf16 storage rounding,
 the relative L2 error, max |ref| and the bound.
 
-    python tests/parity_table.py gpurun_out/parity_errors.jsonl > profiles/parity_errors.md
+    python tests/parity_table.py LOG.jsonl "COMMAND" > profiles/parity_errors.md
+
+where LOG.jsonl is the file the run named in LIBRA_PARITY_LOG and COMMAND the
+command line of that run (printed in the table's header).
 """
 import collections
 import json
@@ -48,4 +51,4 @@ def main(path, command):
 
 if __name__ == "__main__":
     main(sys.argv[1], sys.argv[2] if len(sys.argv) > 2 else
-         "LIBRA_PARITY_LOG=gpurun_out/parity_errors.jsonl python -m pytest tests -m gpu")
+         f"LIBRA_PARITY_LOG={sys.argv[1]} python -m pytest tests -m gpu")
