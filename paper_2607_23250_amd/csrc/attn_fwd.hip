@@ -372,12 +372,15 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     __syncthreads();
     for (int b = kb0; b < nkb; ++b) {
       const int buf = (b - kb0) & 1;
-      // the next block's K rows now, its V rows after this block's S^T
-      // products (the other workgroup on the CU keeps the matrix cores busy
-      // while this one waits to issue)
+      // the next block's K rows after this block's S^T products, its V rows
+      // after the softmax (the other workgroup on the CU keeps the matrix
+      // cores busy while this one waits to issue; waves without rows in this
+      // block post both at once)
       const bool more = b + 1 < nkb;
-      if (more) issue(b + 1, buf ^ 1, 0);
-      if (b >= wave_nkb && more) issue(b + 1, buf ^ 1, 1);
+      if (b >= wave_nkb && more) {
+        issue(b + 1, buf ^ 1, 0);
+        issue(b + 1, buf ^ 1, 1);
+      }
       if (b < wave_nkb) {
         const bf16 *Ks = smem + buf * S::STAGE;
         const bf16 *Vs = Ks + S::K_EL;
@@ -389,7 +392,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
             s[t] = mfma32(*reinterpret_cast<const bf16x8 *>(kp + koff[c]), qf[c], s[t]);
           });
         });
-        if (more) issue(b + 1, buf ^ 1, 1);
+        if (more) issue(b + 1, buf ^ 1, 0);
         // keys past the row are masked only in blocks that reach past the
         // wave's first row (the diagonal block of each row)
         if (b * kFwdBN + kFwdBN - 1 > wave_qmin) {
@@ -437,6 +440,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
           expo(-m_run);
         }
         l_run += ps;
+        if (more) issue(b + 1, buf ^ 1, 1);
         // O^T += V^T P^T; key chunk c = 16 keys from tile row 16 c
         static_for<D / 32>([&](auto dt) {
           static_for<4>([&](auto c) {
