@@ -203,7 +203,8 @@ __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
         // block i landed for every wave; dS^T of block i - 1 is in its slot
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         barrier_nofence();
-        if (i < wave_nkb) {
+        // a part of a split item ends at nkb below the wave's last block
+        if (i < wave_nkb && i < nkb) {
           bf16 *slot = ds_slots + (i & 1) * S::DS_EL;
           if (i * kFwdBN + kFwdBN - 1 > wave_qmin)   // reaches past the wave's first row
             d_run += block(std::true_type{}, i, slot);

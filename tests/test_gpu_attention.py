@@ -123,6 +123,57 @@ def test_bwd_split_k_few_rows_long_sample(h_q, h_kv, d):
     check("dV fp32", to_np(dv32), dV)
 
 
+@pytest.mark.parametrize("h_q,h_kv,d", [(4, 2, 128), (4, 1, 64)])
+def test_bwd_split_k_parts_sum_their_own_keys(h_q, h_kv, d):
+    """Split K in the backward with the rows' attention held by every 32nd
+    key block (blocks 28 mod 32: the fourth-last block of each 32-block key
+    range), and dP taking different values on those blocks.  Each part of a
+    split dQ item adds up dS over its key blocks for the D correction that
+    the dK / dV kernel reads.  Here, counting the fourth-last block of every
+    part but the last twice (a CPU emulation with these inputs) moves dK by
+    0.16 (d = 128) and 0.24 (d = 64) in max-abs and by 0.24 in relative L2,
+    far beyond the bounds.  Rows L - 256 .. L of a 65,536-token sample, query heads 0 and 1;
+    small noise in every tensor."""
+    L = 65536
+    tiles, pos = _span_tiles([(L - 256, L, 0, 2)])
+    n_q = len(pos)
+    say(f"[bwd split K, concentrated attention] sample {L} rows={n_q} heads=({h_q},{h_kv}) d={d}")
+    gen = torch.Generator().manual_seed(31)
+    noise = lambda *shape: 0.1 * torch.randn(*shape, generator=gen)
+    blk = torch.arange(L) // 64
+    held = blk % 32 == 28
+    sign = torch.where(blk // 32 >= 30, -15.0, 1.0)
+    k = noise(L, h_kv, d)
+    k[:, :, 0] = torch.where(held, 11.0, -11.0)[:, None]
+    k[:, :, 2] = torch.where(held, sign, 0.0)[:, None]   # dQ of order 1
+    v = noise(L, h_kv, d)
+    v[:, :, 1] = torch.where(held, sign, 0.0)[:, None]
+    q = noise(n_q, h_q, d)
+    q[:, :, 0] = 8.0
+    do = torch.zeros(n_q, h_q, d)
+    do[:, :2] = noise(n_q, 2, d)
+    do[:, :2, 1] = 1.0
+    q, k, v, do = (t.to(torch.bfloat16) for t in (q, k, v, do))
+    cu = torch.tensor([0, L], dtype=torch.int64, device=DEV)
+    qd, kd, vd, dod = _dev(q, k, v, do)
+    td = pl.tiles_to_device(tiles, DEV)
+    o, lse = pl.libra_attn_fwd(qd, kd, vd, cu, td)
+    dq, dk, dv = pl.libra_attn_bwd(qd, kd, vd, o, lse, dod, cu, td)
+    dk32 = torch.zeros(kd.shape, dtype=torch.float32, device=DEV)
+    dv32 = torch.zeros_like(dk32)
+    pl.libra_attn_bwd(qd, kd, vd, o, lse, dod, cu, td, dk=dk32, dv=dv32, accumulate=True)
+    torch.cuda.synchronize()
+    O, LSE = oa.attention_fwd(q, k, v, [L], pos, heads=range(2))
+    check("O", to_np(o)[:, :2], O[:, :2], bf16_out=True)
+    check("LSE", to_np(lse)[:2], LSE[:2], (LSE_TOL, 1e-4))
+    dQ, dK, dV = oa.attention_bwd(q, k, v, do, [L], pos)
+    check("dQ covered", to_np(dq)[:, :2], np.asarray(dQ)[:, :2], bf16_out=True)
+    check("dK", to_np(dk), dK, bf16_out=True)
+    check("dV", to_np(dv), dV, bf16_out=True)
+    check("dK fp32", to_np(dk32), dK)
+    check("dV fp32", to_np(dv32), dV)
+
+
 @pytest.mark.parametrize("seed", range(16))
 def test_bwd_small_random(seed):
     w = wl.small_random(seed)
