@@ -3,8 +3,8 @@
 // dP^T - D = [V | 1] [dO | -D]^T (lane = query; D enters as one extra
 // k-block, as in the dK / dV kernel), forms dS^T = P^T * (dP^T - D) on the
 // VALU and accumulates dQ^T += K^T dS^T, with the key blocks staged in a
-// 4-deep LDS ring.  Producer and consumer waves split this work (see the
-// kernel).
+// 4-deep LDS ring.  Two waves share each (head, 32 rows) slice, one per
+// 32-key half of every block (see the kernel).
 //
 // It runs before the dK / dV kernel and hands it D: D = rowsum(dO * O) equals
 // sum_k P_k dP_k (O = sum_k P_k V_k), which this kernel has in fp32 for every
@@ -28,22 +28,23 @@ struct DqShape {
   static constexpr int K_EL = kFwdBN * D;
   static constexpr int STAGE = 2 * K_EL;      // K and V rows of one key block
   static constexpr int NSTAGE = 4;            // LDS ring of key blocks
-  static constexpr int DS_EL = 4 * 64 * 8;    // dS^T of one slice and block (4 KiB)
-  static constexpr int NSLOT = 2;             // dS^T hand-over slots per slice
-  static constexpr int NK = kFwdBN * KC / 64 / kWaves;   // wave loads per K (V) tile
-  // at d = 128 the dynamic LDS is exactly the 160 KiB of a CU
-  static constexpr size_t SMEM = (NSTAGE * STAGE + kWaves * NSLOT * DS_EL) * sizeof(bf16);
+  static constexpr int NW = 2 * kWaves;       // waves of the workgroup
+  static constexpr int NK = kFwdBN * KC / 64 / NW;   // wave loads per K (V) tile
+  static constexpr size_t SMEM = NSTAGE * STAGE * sizeof(bf16);
+  // the item-end exchange of the second waves' dQ^T and dS sums fits the ring
+  static_assert(kWaves * 64 * (D / 2 + 1) * sizeof(float) <= SMEM, "exchange fits the ring");
 };
 
-// Eight waves, two per SIMD, in pairs that share a (query head, 32 rows)
-// slice of the work item: the producer (waves 0..3) computes S^T and
-// dP^T - D on the matrix cores and dS^T on the VALU and hands dS^T over
-// through LDS; the consumer (waves 4..7, on the producer's SIMD) stages the
-// K / V blocks and accumulates dQ^T += K^T dS^T one block behind.  While one
-// wave of a SIMD is on the VALU, the other keeps the matrix cores busy, and
-// the copies no longer stall the wave that does the VALU work.  One barrier
-// per block; the K / V ring has four stages (producers read block i while
-// consumers read block i - 1, and blocks i + 1 and i + 2 land).
+// Eight waves, two per (query head, 32 rows) slice of the work item: wave
+// w + 4 h of slice w takes keys 32 h .. 32 h + 31 of every 64-key block.  Per
+// block each wave computes S^T and dP^T - D of its 32 keys, dS^T on the VALU
+// (interleaved with its own products) and dQ^T += K^T dS^T, the last one block
+// behind, with its dS^T straight from registers (the S^T rows are ordered so
+// that its accumulators are the B operand of the dQ^T products).  The two
+// halves of a slice add up their dQ^T and sums of dS at the end of the item.
+// One barrier per block; a 4-stage K / V ring (block i read by the S^T and
+// dP^T products, block i - 1 by the dQ^T products, blocks i + 1 and i + 2
+// land).
 template <int D>
 __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
     const bf16 *__restrict__ q, const bf16 *__restrict__ dout, const bf16 *__restrict__ k,
@@ -54,25 +55,36 @@ __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
     float *__restrict__ parts) {
   using S = DqShape<D>;
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
-  // the item index lives in the first dS^T slot, free between items
-  int32_t &s_item = *reinterpret_cast<int32_t *>(smem + S::NSTAGE * S::STAGE);
+  __shared__ int32_t s_item;
   const int tid = threadIdx.x, l = tid & 63, ln = l & 31, kg = l >> 5;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
-  const bool producer = wv < kWaves;
   const int w = wv & (kWaves - 1);                         // slice of the item
-  // the XCD under round-robin dispatch (the value xcd_of_workgroup() reads;
-  // this form gives this kernel the faster schedule)
+  const int hf = wv / kWaves;                              // 32-key half of each block
   int q_serve = blockIdx.x % kXcds, q_left = kXcds;
-  bf16 *ds_slots = smem + S::NSTAGE * S::STAGE + w * S::NSLOT * S::DS_EL;
-  // scale of -D in the dK / dV kernel's fp16 operands (s_o * s_v, fp16_scale)
   const float s_ov = fp16_scale((uint32_t)hdr[kMaxAbs + 1], true) *
                      fp16_scale((uint32_t)hdr[kMaxAbs + 3], true);
-  // staging (consumers): wave load u covers rows (w + 4u) * 64 / KC + l / KC
-  // of a tile
-  static_assert(S::NK % 2 == 0, "staging copies go four at a time");
-  auto kst = [&](int u) { return (w + kWaves * u) * (64 / S::KC) + l / S::KC; };
-  const int prow = perm32(ln);
-  // A operand of the augmented k-block of dP^T: ones in k = 0, 1, 2
+  // staging: wave load u covers rows (wv + 8u) * 64 / KC + l / KC of a tile
+  auto kst = [&](int u) { return (wv + S::NW * u) * (64 / S::KC) + l / S::KC; };
+  uint32_t k_lane[S::NK];
+  static_for<S::NK>([&](auto u) {
+    const int r = kst(u);
+    k_lane[u] = 2u * (uint32_t)(r * h_kv * D + 8 * swt<S::KC>(r, l % S::KC));
+  });
+  const int prow = perm32(ln) + 32 * hf;
+  int koff[D / 16];
+  static_for<D / 16>([&](auto c) { koff[c] = prow * D + 8 * swt<S::KC>(prow, 2 * c + kg); });
+  // transpose reads of the K^T operands (key chunk 2 hf + c of the block)
+  int troff[D / 32][2];
+  {
+    const int grp = l >> 4, i = (l & 15) >> 2, r = l & 3;
+    static_for<D / 32>([&](auto dt) {
+      static_for<2>([&](auto h2) {
+        const int row = 8 * (grp >> 1) + 4 * h2 + i;
+        const int chunk = 4 * dt + 2 * (grp & 1) + (r & 1);
+        troff[dt][h2] = row * D + 8 * swt<S::KC>(row, chunk) + 4 * (r >> 1);
+      });
+    });
+  }
   bf16x8 ones3;
   static_for<8>([&](auto i) { ones3[int(i)] = bf16(kg == 0 && i < 3 ? 1.f : 0.f); });
 
@@ -82,37 +94,37 @@ __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
     const int idx = __builtin_amdgcn_readfirstlane(s_item);
     if (idx < 0) break;
     const FwdItem it = items[idx];
-    const int64_t key0 = cu[it.sample];
+    const int key0 = (int)cu[it.sample];   // n_kv < 2^31 (checked at the boundary)
     const int head = it.head0 + (w % it.nh);
     const int wrow0 = (w / it.nh) * kRows;
     const int wrows = min(max(it.nrows - wrow0, 0), kRows);
     const bool active = wrows > 0;
     const int my_r = active ? min(ln, wrows - 1) : 0;
-    const int64_t row = (int64_t)it.q_row0 + wrow0 + my_r;
+    const int row = it.q_row0 + wrow0 + my_r;   // Q rows are indexed in 32 bits (FwdItem)
     const int qloc = it.q_loc0 + wrow0 + my_r;
     const int wave_qmin = it.q_loc0 + wrow0;
     const int kb0 = it.kb0, nkb = it.kb1;   // key blocks [kb0, nkb)
     const int wave_nkb = active ? (it.q_loc0 + wrow0 + wrows - 1) / kFwdBN + 1 : 0;
+    const int pend = min(wave_nkb, nkb);    // this wave's blocks [kb0, pend)
 
-    // global -> LDS (consumers), asynchronous: K and V rows of key block b
-    // (keys past the buffer read the last key instead; they are masked);
-    // k_lane[u] is the lane's byte offset from the block's first row
-    auto issue = [&](int b, const uint32_t (&k_lane)[S::NK]) {
+    // global -> LDS, asynchronous: K and V rows of key block b (keys past the
+    // buffer read the last key instead; they are masked)
+    auto issue = [&](int b) {
       bf16 *Ks = smem + (b % S::NSTAGE) * S::STAGE;
       bf16 *Vs = Ks + S::K_EL;
-      const int64_t kbase = key0 + (int64_t)b * kFwdBN;
+      const int kbase = key0 + b * kFwdBN;
       if (kbase + kFwdBN <= n_kv) {
         const size_t off = ((size_t)kbase * h_kv + it.g) * D;
-        const uint32_t lk = lds_addr(Ks) + 1024u * w, lv = lds_addr(Vs) + 1024u * w;
-        static_for<S::NK / 2>([&](auto h) {
-          constexpr uint32_t d0 = 2 * h * kWaves * 1024u, d1 = d0 + kWaves * 1024u;
-          g2l16x4(k + off, v + off, k_lane[2 * h], k_lane[2 * h + 1], lk + d0, lk + d1, lv + d0,
-                  lv + d1);
-        });
+        const uint32_t lk = lds_addr(Ks) + 1024u * wv, lv = lds_addr(Vs) + 1024u * wv;
+        if constexpr (S::NK == 2)
+          g2l16x4(k + off, v + off, k_lane[0], k_lane[1], lk, lk + S::NW * 1024u, lv,
+                  lv + S::NW * 1024u);
+        else
+          g2l16x2(k + off, v + off, k_lane[0], lk, lv);
         return;
       }
       static_for<S::NK>([&](auto u) {
-        const int wl = w + kWaves * u;
+        const int wl = wv + S::NW * u;
         const int r = kst(u);
         int64_t key = key0 + (int64_t)b * kFwdBN + r;
         key = key < n_kv ? key : n_kv - 1;
@@ -122,178 +134,186 @@ __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
       });
     };
 
-    if (producer) {
-      // per-lane LDS offsets (elements) of the K / V rows perm32(ln) for S^T and dP^T
-      int koff[D / 16];
-      static_for<D / 16>([&](auto c) { koff[c] = prow * D + 8 * swt<S::KC>(prow, 2 * c + kg); });
-      // ---- producer: Q and dO rows of this lane's query (B operands),
-      // LSE log2(e), and -D (pre-pass value) for dP^T's augmented k-block
-      bf16x8 qf[D / 16], of[D / 16], dneg;
-      float l2 = 0.f, dd_q = 0.f;
-      if (active) {
-        const size_t off = ((size_t)row * h_q + head) * D + 8 * kg;
+    // Q and dO rows of this lane's query (B operands), LSE log2(e), and -D
+    // (pre-pass value) for dP^T's augmented k-block
+    bf16x8 qf[D / 16], of[D / 16], dneg;
+    float l2 = 0.f, dd_q = 0.f;
+    if (active) {
+      const size_t off = ((size_t)row * h_q + head) * D + 8 * kg;
 #pragma unroll
-        for (int c = 0; c < D / 16; ++c) {
-          qf[c] = *reinterpret_cast<const bf16x8 *>(q + off + 16 * c);
-          of[c] = *reinterpret_cast<const bf16x8 *>(dout + off + 16 * c);
-        }
-        const float *st = stats + ((size_t)head * (nq_pad / kRows) + row / kRows) * 2 * kRows;
-        l2 = st[row % kRows];
-        dd_q = st[kRows + row % kRows];
+      for (int c = 0; c < D / 16; ++c) {
+        qf[c] = *reinterpret_cast<const bf16x8 *>(q + off + 16 * c);
+        of[c] = *reinterpret_cast<const bf16x8 *>(dout + off + 16 * c);
       }
-      split3(kg == 0 ? -dd_q : 0.f, dneg);
-      const float neg_l2 = -l2;
-      wait_vm_known();
-      // S^T and dP^T - D of block b (keys on M, queries on N), then
-      // dS^T = P^T * (dP^T - D), P^T = exp2(S^T c2 - LSE log2 e) (with MASK,
-      // keys after the lane's query give P = 0), into hand-over slot `slot`.
-      // Returns this lane's sum of dS over the block.
-      auto block = [&](auto mask_t, int b, bf16 *slot) {
-        constexpr bool MASK = decltype(mask_t)::value;
-        constexpr int NC = D / 16, NM = 4 * NC, AHEAD = 4;
-        const bf16 *Ks = smem + (b % S::NSTAGE) * S::STAGE, *Vs = Ks + S::K_EL;
-        f32x16 sa[2], pa[2];
-        // MFMA i = 2 NC t + 2 c + kind (kind 0: S^T from K, 1: dP^T from V);
-        // each operand is read AHEAD MFMAs before its product
-        bf16x8 op[NM];
-        auto rd = [&](auto i) {
-          constexpr int t = i / (2 * NC), c = (i % (2 * NC)) / 2, kind = i % 2;
-          op[i] = *reinterpret_cast<const bf16x8 *>((kind ? Vs : Ks) + 32 * t * D + koff[c]);
-        };
-        bf16x8 dsf[4];
-        float dsum = 0.f;
-        auto elem = [&](auto t, auto r) {
-          float x = __builtin_fmaf(sa[t][int(r)], c2, neg_l2);
-          if constexpr (MASK) {
-            const int kl = b * kFwdBN + 32 * t + 16 * (r >> 3) + 8 * kg + (r & 7);
-            x = kl > qloc ? -INFINITY : x;
-          }
-          const float ds = fast_exp2(x) * pa[t][int(r)];
-          dsum += ds;
-          dsf[2 * t + (r >> 3)][r & 7] = static_cast<bf16>(ds);
-        };
-        static_for<AHEAD>([&](auto i) { rd(i); });
+      const float *st = stats + ((size_t)head * (nq_pad / kRows) + row / kRows) * 2 * kRows;
+      l2 = st[row % kRows];
+      dd_q = st[kRows + row % kRows];
+    }
+    split3(kg == 0 ? -dd_q : 0.f, dneg);
+    const float neg_l2 = -l2;
+    wait_vm_known();
+    if (kb0 < nkb) issue(kb0);
+    if (kb0 + 1 < nkb) issue(kb0 + 1);
+
+    f32x16 acc[D / 32];
+    static_for<D / 32>([&](auto dt) { acc[dt] = mfma_zero(); });
+    bf16x8 dsf[2];          // dS^T of the previous block (B operands, two 16-key chunks)
+    float d_run = 0.f;      // this lane's sum of dS over its keys
+    // Block b: S^T (8 products at d = 128), the copies of block b + 2 (COPY),
+    // dP^T - D (9 products, with the exponentials of P^T on the VALU), then
+    // dQ^T += K^T dS^T of block b - 1 (PREV, 8 products) with dS^T of block b
+    // on the VALU.  The copies wait behind the other waves' in the memory
+    // path; posted here, the S^T products of the wave are already queued on
+    // the matrix cores.
+    auto block = [&](auto prev_t, auto mask_t, int b, bool copy) {
+      constexpr bool PREV = decltype(prev_t)::value, MASK = decltype(mask_t)::value;
+      constexpr int NC = D / 16, AHEAD = 3;
+      const bf16 *Ks = smem + (b % S::NSTAGE) * S::STAGE, *Vs = Ks + S::K_EL;
+      f32x16 sa, pa;
+      bf16x8 op[2 * NC];   // MFMA i < NC: S^T from K; NC + c: dP^T from V
+      auto rd = [&](auto i) {
+        constexpr int kind = i / NC, c = i % NC;
+        op[i] = *reinterpret_cast<const bf16x8 *>((kind ? Vs : Ks) + koff[c]);
+      };
+      static_for<AHEAD>([&](auto i) { rd(i); });
+      __builtin_amdgcn_sched_barrier(0);
+      static_for<2 * NC>([&](auto i) {
+        constexpr int kind = i / NC, c = i % NC;
+        if constexpr (kind == 0)
+          sa = mfma32(op[i], qf[c], c == 0 ? mfma_zero_c() : sa);
+        else
+          pa = mfma32(op[i], of[c], c == 0 ? mfma32(ones3, dneg, mfma_zero_c()) : pa);
+        if constexpr (i + AHEAD < 2 * NC) rd(std::integral_constant<int, i + AHEAD>{});
+        if constexpr (i == NC - 1)
+          if (copy) issue(b + 2);
+        if constexpr (kind == 1) {
+          // P^T = exp2(S^T c2 - LSE log2 e), 16 / NC elements per product
+          static_for<16 / NC>([&](auto e) {
+            constexpr int r = (16 / NC) * c + e;
+            float x = __builtin_fmaf(sa[r], c2, neg_l2);
+            if constexpr (MASK) {
+              const int kl = b * kFwdBN + 32 * hf + 16 * (r >> 3) + 8 * kg + (r & 7);
+              x = kl > qloc ? -INFINITY : x;
+            }
+            sa[r] = fast_exp2(x);   // P^T in place
+          });
+        }
         __builtin_amdgcn_sched_barrier(0);
-        // the products of the second 32-key tile carry the VALU work of the
-        // first
-        constexpr int EPM = 16 / (2 * NC);   // elements of tile 0 per product of tile 1
-        static_for<NM>([&](auto i) {
-          constexpr int t = i / (2 * NC), c = (i % (2 * NC)) / 2, kind = i % 2;
-          if constexpr (kind == 0)
-            sa[t] = mfma32(op[i], qf[c], c == 0 ? mfma_zero_c() : sa[t]);
-          else
-            pa[t] = mfma32(op[i], of[c],
-                           c == 0 ? mfma32(ones3, dneg, mfma_zero_c()) : pa[t]);
-          if constexpr (i + AHEAD < NM) rd(std::integral_constant<int, i + AHEAD>{});
-          if constexpr (t == 1)
-            static_for<EPM>([&](auto e) {
-              elem(std::integral_constant<int, 0>{},
-                   std::integral_constant<int, EPM * (i - 2 * NC) + e>{});
-            });
+      });
+      // dS^T = P^T * (dP^T - D) of block b, under the dQ^T products of block b - 1
+      bf16x8 dn[2];
+      float dsum = 0.f;
+      auto ds_elem = [&](auto rc) {
+        constexpr int r = decltype(rc)::value;
+        const float ds = sa[r] * pa[r];
+        dsum += ds;
+        dn[r >> 3][r & 7] = static_cast<bf16>(ds);
+      };
+      if constexpr (PREV) {
+        const bf16 *Kp = smem + ((b - 1) % S::NSTAGE) * S::STAGE + 32 * hf * D;
+        constexpr int NT = D / 32, NQ = 2 * NT, TA = 3;   // MFMA j = NT c + dt
+        bf16x8 tp[NQ];
+        auto rt = [&](auto j) {
+          const bf16 *base = Kp + 16 * (j / NT) * D;
+          tp[j] = lds_tr16x2(base + troff[j % NT][0], base + troff[j % NT][1]);
+        };
+        static_for<TA>([&](auto j) { rt(j); });
+        static_for<NQ>([&](auto j) {
+          acc[j % NT] = mfma32(tp[j], dsf[j / NT], acc[j % NT]);
+          if constexpr (j + TA < NQ) rt(std::integral_constant<int, j + TA>{});
+          static_for<16 / NQ>([&](auto e) {
+            ds_elem(std::integral_constant<int, (16 / NQ) * j + e>{});
+          });
           __builtin_amdgcn_sched_barrier(0);
         });
-        static_for<16>([&](auto r) { elem(std::integral_constant<int, 1>{}, r); });
-        static_for<4>([&](auto c) {
-          *reinterpret_cast<bf16x8 *>(slot + (c * 64 + l) * 8) = dsf[c];
-        });
-        return dsum;
-      };
-      float d_run = 0.f;   // this lane's half of sum_k dS_k over the row's keys
-      for (int i = kb0; i <= nkb; ++i) {
-        // block i landed for every wave; dS^T of block i - 1 is in its slot
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        barrier_nofence();
-        // a part of a split item ends at nkb below the wave's last block
-        if (i < wave_nkb && i < nkb) {
-          bf16 *slot = ds_slots + (i & 1) * S::DS_EL;
-          if (i * kFwdBN + kFwdBN - 1 > wave_qmin)   // reaches past the wave's first row
-            d_run += block(std::true_type{}, i, slot);
-          else
-            d_run += block(std::false_type{}, i, slot);
-        }
+      } else {
+        static_for<16>([&](auto r) { ds_elem(r); });
       }
-      // D_exact = D + sum_k dS_k (sum_k P_k = 1): the -D record of the dK / dV
-      // kernel's augmented operands for this (row, head)
-      const float d_part = row_sum2(d_run);
-      const float d_exact = dd_q + d_part;
-      if (it.slot >= 0) {
-        // a part of a split item: its sum of dS, merged by bwd_dq_combine_kernel
-        if (active && ln < wrows && kg == 0)
-          parts[(size_t)it.slot * fwd_part_floats(D) + (size_t)kFwdPartRows * D + w * kRows + ln] =
-              d_part;
-      } else if (active && ln < wrows && kg == 0) {
-        f16x8 rec;
-        split3h(-d_exact * s_ov, rec);
-        *reinterpret_cast<f16x8 *>(aug + ((size_t)head * (nq_pad / kRows) + row / kRows) * kAugEl +
-                                   kAugEl / 2 + 8 * perm32((int)(row % kRows))) = rec;
-      }
-    } else {
-      // ---- consumer: stages K / V one block ahead, accumulates dQ^T; the
-      // per-lane LDS offsets of the transpose reads of the K tile (K^T)
-      int troff[D / 32][2];
-      {
-        const int grp = l >> 4, i = (l & 15) >> 2, r = l & 3;
-        static_for<D / 32>([&](auto dt) {
-          static_for<2>([&](auto hf) {
-            const int row = 8 * (grp >> 1) + 4 * hf + i;
-            const int chunk = 4 * dt + 2 * (grp & 1) + (r & 1);
-            troff[dt][hf] = row * D + 8 * swt<S::KC>(row, chunk) + 4 * (r >> 1);
-          });
-        });
-      }
-      uint32_t k_lane[S::NK];
-      static_for<S::NK>([&](auto u) {
-        const int r = kst(u);
-        k_lane[u] = 2u * (uint32_t)(r * h_kv * D + 8 * swt<S::KC>(r, l % S::KC));
+      dsf[0] = dn[0];
+      dsf[1] = dn[1];
+      return dsum;
+    };
+    // dQ^T += K^T dS^T of the wave's last block
+    auto flush = [&](int b) {
+      const bf16 *Kp = smem + (b % S::NSTAGE) * S::STAGE + 32 * hf * D;
+      static_for<2 * (D / 32)>([&](auto j) {
+        const bf16 *base = Kp + 16 * (j & 1) * D;
+        acc[j >> 1] = mfma32(lds_tr16x2(base + troff[j >> 1][0], base + troff[j >> 1][1]),
+                             dsf[j & 1], acc[j >> 1]);
       });
-      f32x16 acc[D / 32];
-      static_for<D / 32>([&](auto dt) { acc[dt] = mfma_zero(); });
-      if (kb0 < nkb) issue(kb0, k_lane);
-      if (kb0 + 1 < nkb) issue(kb0 + 1, k_lane);
-      for (int i = kb0; i <= nkb; ++i) {
-        // this wave's copies of block i (block i + 1's may stay in flight)
-        if (i + 1 < nkb) wait_vm_n<2 * S::NK>();
-        else wait_vm();
-        barrier_nofence();
-        if (i + 2 < nkb) issue(i + 2, k_lane);
-        const int b = i - 1;
-        if (b >= kb0 && b < wave_nkb) {
-          const bf16 *Ks = smem + (b % S::NSTAGE) * S::STAGE;
-          const bf16 *slot = ds_slots + (b & 1) * S::DS_EL;
-          bf16x8 dsf[4];
-          static_for<4>([&](auto c) {
-            dsf[c] = *reinterpret_cast<const bf16x8 *>(slot + (c * 64 + l) * 8);
-          });
-          // MFMA j = 4 dt + c: key chunk c = 16 keys from tile row 16 c;
-          // transpose operands read TA MFMAs ahead
-          constexpr int NQ = 4 * (D / 32), TA = 3;
-          bf16x8 tp[NQ];
-          auto rt = [&](auto j) {
-            const bf16 *base = Ks + 16 * (j & 3) * D;
-            tp[j] = lds_tr16x2(base + troff[j >> 2][0], base + troff[j >> 2][1]);
-          };
-          static_for<TA>([&](auto j) { rt(j); });
-          static_for<NQ>([&](auto j) {
-            acc[j >> 2] = mfma32(tp[j], dsf[j & 3], acc[j >> 2]);
-            if constexpr (j + TA < NQ) rt(std::integral_constant<int, j + TA>{});
-            __builtin_amdgcn_sched_barrier(0);
-          });
+    };
+    using T_ = std::true_type;
+    using F_ = std::false_type;
+    // blocks from (wave_qmin + 1) / 64 on reach past the wave's first row
+    const int unmasked_end = (wave_qmin + 1) / kFwdBN;
+    // iteration i: this wave's copies of block i (block i + 1's may stay in
+    // flight), the barrier, then the copies of block i + 2: here for a wave
+    // without a block in this iteration, else inside block() (returns true)
+    auto step = [&](int i) {
+      if (i + 1 < nkb) wait_vm_n<2 * S::NK>();
+      else wait_vm();
+      barrier_nofence();
+      const bool copy = i + 2 < nkb, in_block = copy && i < pend;
+      if (copy && !in_block) issue(i + 2);
+      return in_block;
+    };
+    // the first block, the unmasked ones, then the masked ones and the last
+    // dQ^T products: one iteration per i in [kb0, nkb] for every wave
+    int i = kb0;
+    bool cp = step(i);
+    if (i < pend)
+      d_run += i < unmasked_end ? block(F_{}, F_{}, i, cp) : block(F_{}, T_{}, i, cp);
+    const int pipe_end = min(pend, unmasked_end);
+    for (++i; i < pipe_end; ++i) {
+      cp = step(i);
+      d_run += block(T_{}, F_{}, i, cp);
+    }
+    for (; i <= nkb; ++i) {
+      cp = step(i);
+      if (i < pend)
+        d_run += block(T_{}, T_{}, i, cp);
+      else if (i == pend && pend > kb0)
+        flush(i - 1);
+    }
+
+    // the second half of each slice hands its dQ^T and sum of dS to the first
+    // through the ring (every wave is past its last LDS read of the ring)
+    float d_half = row_sum2(d_run);
+    __syncthreads();
+    float *ex = reinterpret_cast<float *>(smem) + (size_t)w * 64 * (D / 2 + 1);
+    if (hf == 1) {
+      static_for<D / 32>([&](auto dt) {
+        static_for<16>([&](auto r) { ex[(dt * 16 + r) * 64 + l] = acc[dt][int(r)]; });
+      });
+      ex[(D / 2) * 64 + l] = d_half;
+    }
+    __syncthreads();
+    if (hf == 0) {
+      static_for<D / 32>([&](auto dt) {
+        static_for<16>([&](auto r) { acc[dt][int(r)] += ex[(dt * 16 + r) * 64 + l]; });
+      });
+      d_half += ex[(D / 2) * 64 + l];
+      const float d_exact = dd_q + d_half;
+      if (it.slot >= 0) {
+        // a part of a split item: unscaled fp32 dQ and its sum of dS, merged by
+        // bwd_dq_combine_kernel
+        if (active && ln < wrows) {
+          float *op = parts + (size_t)it.slot * fwd_part_floats(D) + (size_t)(w * kRows + ln) * D +
+                      8 * kg;
+#pragma unroll
+          for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+              float4 *dst = reinterpret_cast<float4 *>(op + 32 * dt + 16 * hh);
+              dst[0] = make_float4(acc[dt][8 * hh], acc[dt][8 * hh + 1], acc[dt][8 * hh + 2],
+                                   acc[dt][8 * hh + 3]);
+              dst[1] = make_float4(acc[dt][8 * hh + 4], acc[dt][8 * hh + 5], acc[dt][8 * hh + 6],
+                                   acc[dt][8 * hh + 7]);
+            }
+          if (kg == 0)
+            parts[(size_t)it.slot * fwd_part_floats(D) + (size_t)kFwdPartRows * D + w * kRows +
+                  ln] = d_half;
         }
-      }
-      if (active && ln < wrows && it.slot >= 0) {
-        // a part of a split item: unscaled fp32 dQ into its partial slot
-        float *op = parts + (size_t)it.slot * fwd_part_floats(D) + (size_t)(w * kRows + ln) * D +
-                    8 * kg;
-#pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt)
-#pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
-            float4 *dst = reinterpret_cast<float4 *>(op + 32 * dt + 16 * hh);
-            dst[0] = make_float4(acc[dt][8 * hh], acc[dt][8 * hh + 1], acc[dt][8 * hh + 2],
-                                 acc[dt][8 * hh + 3]);
-            dst[1] = make_float4(acc[dt][8 * hh + 4], acc[dt][8 * hh + 5], acc[dt][8 * hh + 6],
-                                 acc[dt][8 * hh + 7]);
-          }
       } else if (active && ln < wrows) {
         bf16 *op = dq + ((size_t)row * h_q + head) * D + 8 * kg;
 #pragma unroll
@@ -305,9 +325,18 @@ __global__ __launch_bounds__(2 * kThreads, 1) void attn_bwd_dq_kernel(
             for (int i = 0; i < 8; ++i) ov[i] = static_cast<bf16>(acc[dt][8 * hh + i] * scale);
             *reinterpret_cast<bf16x8 *>(op + 32 * dt + 16 * hh) = ov;
           }
+        // D_exact = D + sum_k dS_k (sum_k P_k = 1): the -D record of the dK / dV
+        // kernel's augmented operands for this (row, head)
+        if (kg == 0) {
+          f16x8 rec;
+          split3h(-d_exact * s_ov, rec);
+          *reinterpret_cast<f16x8 *>(aug + ((size_t)head * (nq_pad / kRows) + row / kRows) *
+                                               kAugEl +
+                                     kAugEl / 2 + 8 * perm32((int)(row % kRows))) = rec;
+        }
       }
     }
-    __syncthreads();   // the ring and the slots are reused by the next item
+    __syncthreads();   // the ring is reused by the next item
   }
 }
 
